@@ -1,0 +1,14 @@
+"""CPU oracle for one mixed scheduler step's attention over a paged KV cache.
+
+TEST INFRASTRUCTURE. Only the tests, the package entry's smoke check and the
+benchmark's CPU-baseline leg may import or run anything here; the product path
+never does. It shares no code with the HIP path: inputs arrive as bf16 bit
+patterns and integer descriptors, and everything else (bf16 decoding, the cache
+semantics, masking, softmax, page addressing) is written out again here, slowly
+and in float64.
+
+Modules:
+  attention -- the attention of a mixed step (chunked prefill rows and decode rows)
+  kv_cache  -- where kv_append puts a step's new keys and values in the page pools
+  policy    -- the P-PAS per-iteration prefill budget (Algorithm 1)
+"""
