@@ -1,0 +1,224 @@
+#!/usr/bin/env python3
+"""Benchmark of one mixed scheduler step's attention over a paged KV cache on one MI355X.
+
+A step is the whole hot path on one batch: the host plan, ppas_kv_append of the
+step's new K/V, and ppas_attn_step (packed attention launch + split merge). Inputs
+are seeded synthetic bf16 N(0,1) values at the Qwen2.5-3B attention shape
+(16 query heads, 2 KV heads, head_dim 128, pages of 16 tokens, permuted block
+table); they are resident in HBM before timing starts. The KV pools rotate over
+several device copies so that no timed step finds its keys in the 256 MB
+Infinity Cache from the previous step.
+
+Prints ONE JSON line. `value` is the algorithmic attention TFLOP/s of the whole
+step (FLOP = 4 * head_dim * n_q_heads * visible (row, key) pairs, softmax not
+counted). `roofline` describes the packed attention kernel, timed with HIP
+events recorded around its launch on its own stream. `cpu_baseline` times the
+CPU oracle on a bounded sample of the same step's rows.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4}
+METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
+PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_GBPS = 8000.0     # MI355X HBM3E
+
+
+class HipEvents:
+    """hipEvent_t pairs through the HIP runtime (timing events on the launch stream)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        ev = ctypes.c_void_p()
+        if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev.value
+
+    def elapsed_ms(self, a, b) -> float:
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, ev):
+        self.hip.hipEventDestroy(ev)
+
+
+def cpu_baseline(data, scale, budget_s: float):
+    """Time the oracle on a bounded sample of the step's rows; returns the JSON object."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle.attention as OA
+    spec = data.spec
+    desc = data.desc
+
+    def sample(frac_rows):
+        rows = []
+        for s, (qs, n, c) in enumerate(desc.tolist()):
+            if n == 1:
+                rows.append(qs)
+            else:
+                k = max(1, int(round(n * frac_rows)))
+                rows += list(range(qs + n - k, qs + n))      # the chunk's last rows: the longest ones
+        return rows
+
+    def flop(rows):
+        pos = {}
+        for s, (qs, n, c) in enumerate(desc.tolist()):
+            for i in range(n):
+                pos[qs + i] = c + i
+        return sum(4.0 * spec.head_dim * spec.n_q_heads * (pos[r] + 1) for r in rows)
+
+    frac = 1.0 / 256
+    while True:
+        rows = sample(frac)
+        t0 = time.perf_counter()
+        OA.step_attention_from_data(data, scale, rows=rows)
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 4 or frac >= 1.0:
+            break
+        frac = min(1.0, frac * max(2.0, budget_s / 2 / max(dt, 1e-3)))
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    f = flop(rows)
+    return {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(rows)} of {spec.n_rows} query rows (every decode row and the last "
+                      f"{frac:.2%} of each prefill chunk), all 16 heads, fp64 NumPy; {f:.3e} FLOP in {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mbt2048")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
+              "multi-GPU mode; see the sharding notes in DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import inputs as I
+    from paper_2608_15171_amd import metrics as M
+    from paper_2608_15171_amd import ppas
+    from paper_2608_15171_amd.step import DeviceStep
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    spec = I.CONFIGS[WORKLOADS[args.workload]](args.seed)
+    data = I.make_step_data(spec, args.seed)
+    bt, npages = I.make_block_table(spec, args.seed, permute=True)
+    ds = DeviceStep(data, bt, npages)
+    ds.fill_history()
+    pool_bytes = ds.k_pages.numel() * 2 * 2
+    copies = max(2, min(8, math.ceil(1.0e9 / pool_bytes) + 1))
+    pools = [(ds.k_pages, ds.v_pages)] + [(ds.k_pages.clone(), ds.v_pages.clone()) for _ in range(copies - 1)]
+    torch.cuda.synchronize()
+
+    hip = HipEvents()
+    K, W = args.steps, args.warmup
+    ev = [(hip.create(), hip.create()) for _ in range(K)]
+    ka = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+
+    def one_step(i, timed):
+        ds.k_pages, ds.v_pages = pools[i % copies]
+        if timed:
+            ka[i][0].record()
+        ds.append()
+        if timed:
+            ka[i][1].record()
+            ppas.set_profile_events(*ev[i])
+        ds.attend()
+        if timed:
+            ppas.set_profile_events(None, None)
+
+    for i in range(W):
+        one_step(i, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        one_step(i, True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    ms_step = (t1 - t0) / K * 1e3
+    attn_ms = [hip.elapsed_ms(a, b) for a, b in ev]
+    app_ms = [a.elapsed_time(b) for a, b in ka]
+    for a, b in ev:
+        hip.destroy(a)
+        hip.destroy(b)
+    k_ms = float(np.mean(attn_ms))
+
+    F = M.flops(spec)
+    B = M.attn_bytes(spec)
+    t_flop, t_byte = F / (PEAK_TFLOPS * 1e12), B / (PEAK_GBPS * 1e9)
+    bound = "mfma" if t_flop >= t_byte else "hbm"
+    if bound == "mfma":
+        achieved, peak, unit = F / (k_ms * 1e-3) / 1e12, PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = B / (k_ms * 1e-3) / 1e9, PEAK_GBPS, "GB/s"
+
+    rec = {
+        "metric": METRIC,
+        "value": round(F / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": spec.name,
+            "layers": 1,
+            "requests": [[s.n_query, s.cached_len] for s in spec.seqs] if len(spec.seqs) <= 12 else
+                        f"{sum(1 for s in spec.seqs if s.n_query == 1)} decode rows + "
+                        f"{[(s.n_query, s.cached_len) for s in spec.seqs if s.n_query > 1]} (n_query, cached_len) chunks",
+            "query_rows": spec.n_rows,
+            "kv_tokens": int(spec.kv_lens().sum()),
+            "heads": "16q/2kv", "head_dim": 128, "page_size": 16, "block_table": "seeded permutation",
+            "kv_pool_copies_rotated": copies,
+        },
+        "roofline": {
+            "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "kernel": "attn_step_kernel", "kernel_us": round(k_ms * 1e3, 2),
+            "per_launch": {"flop": F, "bytes": B},
+        },
+        "breakdown": {
+            "attn_kernel_us": round(k_ms * 1e3, 2),
+            "attn_kernel_us_min": round(float(np.min(attn_ms)) * 1e3, 2),
+            "kv_append_us": round(float(np.mean(app_ms)) * 1e3, 2),
+            "prefill_tflops_in_kernel": round(M.flops(spec, "prefill") / (k_ms * 1e-3) / 1e12, 2),
+            "decode_kv_gbps_in_kernel": round(M.kv_bytes(spec, "decode") / (k_ms * 1e-3) / 1e9, 2),
+            "step_roofline_us": round(max(t_flop, t_byte) * 1e6, 2),
+        },
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(data, ds.shape.scale, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

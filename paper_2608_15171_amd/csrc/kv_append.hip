@@ -1,0 +1,114 @@
+// Scatter a step's new K/V rows into the paged cache (bit copies).
+//
+// One workgroup per (request, touched page, KV head). The K page of one head is
+// 16 token rows of 256 bytes: thread t copies the 16-byte chunk (slot t/16,
+// features 8(t%16)..) when that slot is one of the step's positions. The V page
+// of one head is 128 feature rows of 16 tokens: thread t owns the chunk
+// (feature t/2, slots 8(t%2)..+7), gathers those slots from the new rows, and
+// stores the whole chunk when all 8 slots are new, else only the new elements.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace ppas {
+
+constexpr int kAppendMaxSeqs = 64;
+
+struct AppendArgs {
+  uint16_t* kp;
+  uint16_t* vp;
+  const uint16_t* kn;
+  const uint16_t* vn;
+  const int32_t* bt;
+  int32_t bt_stride, hkv, n, seq_base;
+  int32_t blk_start[kAppendMaxSeqs + 1];   // prefix sums of touched pages per request
+  int32_t qs[kAppendMaxSeqs], nq[kAppendMaxSeqs], c[kAppendMaxSeqs];
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
+  const int blk = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+  int s = 0;
+  while (s + 1 < a.n && a.blk_start[s + 1] <= blk) ++s;
+  const int c = a.c[s], nq = a.nq[s], qs = a.qs[s];
+  const int lpage = c / kPage + (blk - a.blk_start[s]);
+  const int pos_lo = lpage * kPage;                       // position of slot 0 of this page
+  const int32_t page = a.bt[size_t(a.seq_base + s) * a.bt_stride + lpage];
+  const size_t base = (size_t(page) * a.hkv + g) * kPage * kHeadDim;
+  const size_t row_stride = size_t(a.hkv) * kHeadDim;     // elements between new rows
+
+  // K: slot tid/16, features 8*(tid%16)..+7
+  {
+    const int slot = tid >> 4;
+    const int pos = pos_lo + slot;
+    if (pos >= c && pos < c + nq) {
+      const uint16_t* src = a.kn + size_t(qs + pos - c) * row_stride + g * kHeadDim + 8 * (tid & 15);
+      *reinterpret_cast<u32x4*>(a.kp + base + slot * kHeadDim + 8 * (tid & 15)) = *reinterpret_cast<const u32x4*>(src);
+    }
+  }
+  // V: feature tid/2, slots 8*(tid%2)..+7
+  {
+    const int d = tid >> 1;
+    const int s0 = 8 * (tid & 1);
+    uint16_t* dst = a.vp + base + d * kPage + s0;
+    uint16_t vals[8];
+    int cnt = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int pos = pos_lo + s0 + e;
+      const bool mine = pos >= c && pos < c + nq;
+      vals[e] = mine ? a.vn[size_t(qs + pos - c) * row_stride + g * kHeadDim + d] : uint16_t(0);
+      cnt += mine;
+    }
+    if (cnt == 8) {
+      u32x4 v;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) v[w] = uint32_t(vals[2 * w]) | (uint32_t(vals[2 * w + 1]) << 16);
+      *reinterpret_cast<u32x4*>(dst) = v;
+    } else if (cnt > 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int pos = pos_lo + s0 + e;
+        if (pos >= c && pos < c + nq) dst[e] = vals[e];
+      }
+    }
+  }
+}
+
+hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
+                            const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
+                            int32_t hkv, hipStream_t stream) {
+  for (int32_t s0 = 0; s0 < n_seqs; s0 += kAppendMaxSeqs) {
+    AppendArgs a;
+    a.kp = kp;
+    a.vp = vp;
+    a.kn = kn;
+    a.vn = vn;
+    a.bt = bt;
+    a.bt_stride = bt_stride;
+    a.hkv = hkv;
+    a.seq_base = s0;
+    a.n = 0;
+    int32_t blocks = 0;
+    for (int32_t s = s0; s < n_seqs && s < s0 + kAppendMaxSeqs; ++s) {
+      const int i = a.n++;
+      a.qs[i] = seqs[s].query_start;
+      a.nq[i] = seqs[s].n_query;
+      a.c[i] = seqs[s].cached_len;
+      a.blk_start[i] = blocks;
+      const int first = seqs[s].cached_len / kPage;
+      const int last = (seqs[s].cached_len + seqs[s].n_query - 1) / kPage;
+      blocks += last - first + 1;
+    }
+    a.blk_start[a.n] = blocks;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(blocks, hkv), dim3(256), 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace ppas

@@ -1,0 +1,188 @@
+// Host-side validation and work planning for one mixed step (pure C++, no HIP).
+#include "plan.h"
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <numeric>
+
+namespace ppas {
+
+namespace {
+std::atomic<int32_t> g_prefill_split{0};
+std::atomic<int32_t> g_decode_split{0};
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+}  // namespace
+
+void set_split_keys(int32_t prefill, int32_t decode) {
+  g_prefill_split.store(prefill);
+  g_decode_split.store(decode);
+}
+
+ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
+                     const int32_t* bt_host, int32_t bt_stride, bool check_overlap) {
+  if (!shape) return PPAS_EINVAL;
+  const ppas_shape& s = *shape;
+  if (s.n_q_heads <= 0 || s.n_kv_heads <= 0 || s.head_dim <= 0 || s.page_size <= 0 || s.num_pages <= 0)
+    return PPAS_EINVAL;
+  if (!std::isfinite(s.scale) || !(s.scale > 0.f)) return PPAS_EINVAL;
+  if (s.n_q_heads % s.n_kv_heads != 0) return PPAS_EINVAL;
+  if (s.n_q_heads / s.n_kv_heads != kGroup || s.head_dim != kHeadDim || s.page_size != kPage)
+    return PPAS_EUNSUPPORTED;
+  if (n_seqs < 0) return PPAS_EINVAL;
+  if (n_seqs == 0) return PPAS_OK;
+  if (!seqs) return PPAS_EINVAL;
+  if (bt_stride <= 0) return PPAS_EINVAL;
+  int64_t qs = 0;
+  for (int32_t i = 0; i < n_seqs; ++i) {
+    const ppas_seq& q = seqs[i];
+    if (q.n_query < 1 || q.cached_len < 0) return PPAS_EINVAL;
+    if (q.query_start != qs) return PPAS_EINVAL;
+    const int64_t len = int64_t(q.cached_len) + q.n_query;
+    if (len > INT32_MAX - 64) return PPAS_ERANGE;
+    qs += q.n_query;
+    if (qs > INT32_MAX) return PPAS_ERANGE;
+    if (ceil_div(len, kPage) > bt_stride) return PPAS_EINVAL;
+  }
+  if (!bt_host) return PPAS_OK;
+  for (int32_t i = 0; i < n_seqs; ++i) {
+    const int64_t pages = ceil_div(int64_t(seqs[i].cached_len) + seqs[i].n_query, kPage);
+    const int32_t* row = bt_host + int64_t(i) * bt_stride;
+    for (int64_t j = 0; j < pages; ++j)
+      if (row[j] < 0 || row[j] >= s.num_pages) return PPAS_ERANGE;
+  }
+  if (check_overlap) {
+    // no (page, slot) may be written by two requests of the same step
+    std::vector<uint16_t> used(size_t(s.num_pages), 0);   // bit per slot
+    for (int32_t i = 0; i < n_seqs; ++i) {
+      const int32_t* row = bt_host + int64_t(i) * bt_stride;
+      for (int64_t p = seqs[i].cached_len; p < int64_t(seqs[i].cached_len) + seqs[i].n_query; ++p) {
+        const int32_t page = row[p / kPage];
+        const uint16_t bit = uint16_t(1u << (p % kPage));
+        if (used[page] & bit) return PPAS_EINVAL;
+        used[page] |= bit;
+      }
+    }
+  }
+  return PPAS_OK;
+}
+
+namespace {
+
+struct Job {
+  WorkItem item;
+  double cost;
+  int32_t order_key[4];
+};
+
+}  // namespace
+
+void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, Plan& plan) {
+  plan.items.clear();
+  plan.combine.clear();
+  plan.part_slots = 0;
+  const int hkv = shape.n_kv_heads;
+  if (num_cus <= 0) num_cus = 256;
+
+  // Total work, to size the key splits so that the launch has several
+  // workgroups per compute unit.
+  int64_t prefill_keys = 0, decode_keys = 0;
+  for (int32_t s = 0; s < n_seqs; ++s) {
+    const ppas_seq& q = seqs[s];
+    if (q.n_query == 1) {
+      decode_keys += int64_t(q.cached_len + 1) * hkv;
+    } else {
+      for (int32_t t0 = 0; t0 < q.n_query; t0 += kTilePos)
+        prefill_keys += int64_t(q.cached_len) + std::min(q.n_query, t0 + kTilePos);
+    }
+  }
+  prefill_keys *= hkv;
+
+  int64_t ksp = g_prefill_split.load();
+  if (ksp <= 0) {
+    const int64_t target = int64_t(4) * num_cus;
+    ksp = std::max<int64_t>(1024, ceil_div(prefill_keys, target));
+  }
+  ksp = std::max<int64_t>(kPrefillBlock, ceil_div(ksp, kPrefillBlock) * kPrefillBlock);
+  int64_t ksd = g_decode_split.load();
+  if (ksd <= 0) {
+    const int64_t target = int64_t(2) * num_cus;
+    ksd = std::min<int64_t>(8192, std::max<int64_t>(512, ceil_div(decode_keys, target)));
+  }
+  ksd = std::max<int64_t>(kDecodeBlock, ceil_div(ksd, kDecodeBlock) * kDecodeBlock);
+
+  std::vector<Job> jobs;
+  auto add_unit = [&](int32_t s, int32_t g, int32_t row0, int32_t pos0, int32_t npos, int kind) {
+    const int64_t kend = int64_t(pos0) + npos;        // keys 0..kend-1 are visible to some row
+    int64_t split = kind == kKindDecode ? ksd : ksp;
+    // prefill splits all start at or before pos0, so every row sees a key in every split
+    int64_t nsplit = kind == kKindDecode ? ceil_div(kend, split) : (int64_t(pos0) / split + 1);
+    int32_t part = -1;
+    if (nsplit > 1) {
+      part = int32_t(plan.part_slots);
+      plan.combine.push_back(CombineItem{row0, g, npos, int32_t(nsplit), part, 0, 0, 0});
+      plan.part_slots += nsplit * int64_t(npos) * kGroup;
+    }
+    for (int64_t k = 0; k < nsplit; ++k) {
+      const int64_t lo = k * split;
+      const int64_t hi = (k + 1 == nsplit) ? kend : std::min(kend, (k + 1) * split);
+      Job j;
+      j.item = WorkItem{s, g, row0, pos0, npos | (kind << 16), int32_t(lo), int32_t(hi),
+                        part < 0 ? -1 : int32_t(part + k * int64_t(npos) * kGroup)};
+      // relative cost: a prefill key costs ~128 rows of MFMA work, a decode key
+      // ~512 bytes of HBM traffic; one decode key is about two prefill keys.
+      j.cost = double(hi - lo) * (kind == kKindDecode ? 2.0 : 1.0);
+      j.order_key[0] = s;
+      j.order_key[1] = g;
+      j.order_key[2] = -pos0;
+      j.order_key[3] = int32_t(k);
+      jobs.push_back(j);
+    }
+  };
+  for (int32_t s = 0; s < n_seqs; ++s) {
+    const ppas_seq& q = seqs[s];
+    for (int32_t g = 0; g < hkv; ++g) {
+      if (q.n_query == 1) {
+        add_unit(s, g, q.query_start, q.cached_len, 1, kKindDecode);
+      } else {
+        for (int32_t t0 = 0; t0 < q.n_query; t0 += kTilePos)
+          add_unit(s, g, q.query_start + t0, q.cached_len + t0, std::min(kTilePos, q.n_query - t0), kKindPrefill);
+      }
+    }
+  }
+
+  // Longest first, in cost buckets of 256 keys; inside a bucket keep items of the
+  // same request and KV head together so neighbours share keys in one L2.
+  std::stable_sort(jobs.begin(), jobs.end(), [](const Job& a, const Job& b) {
+    const int64_t ca = int64_t(a.cost) >> 8, cb = int64_t(b.cost) >> 8;
+    if (ca != cb) return ca > cb;
+    for (int i = 0; i < 4; ++i)
+      if (a.order_key[i] != b.order_key[i]) return a.order_key[i] < b.order_key[i];
+    return false;
+  });
+
+  // Workgroup b of a launch runs on XCD b % 8. Hand each XCD runs of 8
+  // consecutive items of the sorted list, with runs dealt round-robin so every XCD
+  // gets the same mix of long and short items: within each block of 64 launch
+  // slots, slot 8v + x takes sorted item 8x + v.
+  const size_t n = jobs.size();
+  plan.items.resize(n);
+  const size_t full = n / 64 * 64;
+  for (size_t b = 0; b < full; ++b) {
+    const size_t x = b % 8, k = b / 8;
+    const size_t src = ((k / 8) * 8 + x) * 8 + (k % 8);
+    plan.items[b] = jobs[src].item;
+  }
+  for (size_t b = full; b < n; ++b) plan.items[b] = jobs[b].item;
+
+  plan.off_items = 0;
+  plan.off_combine = align_up(n * sizeof(WorkItem), 256);
+  plan.off_ml = align_up(plan.off_combine + plan.combine.size() * sizeof(CombineItem), 256);
+  plan.off_acc = align_up(plan.off_ml + size_t(plan.part_slots) * 8, 256);
+  plan.total = align_up(plan.off_acc + size_t(plan.part_slots) * kHeadDim * 4, 256);
+  if (plan.total == 0) plan.total = 256;
+}
+
+}  // namespace ppas

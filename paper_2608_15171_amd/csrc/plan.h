@@ -1,0 +1,56 @@
+// Work list of one mixed step: what each workgroup of the packed attention
+// launch computes, and how split rows are merged afterwards.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "ppas.h"
+
+namespace ppas {
+
+constexpr int kHeadDim = 128;
+constexpr int kPage = 16;
+constexpr int kGroup = 8;          // query heads per KV head
+constexpr int kTilePos = 16;       // positions per prefill tile (x 8 heads = 128 rows)
+constexpr int kPrefillBlock = 64;  // keys per staged K/V block of a prefill tile
+constexpr int kDecodeBlock = 32;   // keys per block of a decode wave
+constexpr int kKindPrefill = 0;
+constexpr int kKindDecode = 1;
+
+// One workgroup's job. A prefill tile covers npos consecutive positions of one
+// request (rows row0..row0+npos-1 of the step, positions pos0..pos0+npos-1) for
+// the 8 query heads of KV head kvh, over keys [key_lo, key_hi). A decode item is
+// the same with npos == 1. part < 0: write bf16 output; else write fp32 partial
+// (max, sum, unnormalised accumulator) for local row r = pos*8 + head at slot part + r.
+struct WorkItem {
+  int32_t seq, kvh, row0, pos0;
+  int32_t npos_kind;               // npos | kind << 16
+  int32_t key_lo, key_hi, part;
+};
+static_assert(sizeof(WorkItem) == 32, "WorkItem is 32 bytes");
+
+// Rows split over nsplit items: split s of local row r sits at slot part + s*npos*8 + r.
+struct CombineItem {
+  int32_t row0, kvh, npos, nsplit, part, pad0, pad1, pad2;
+};
+static_assert(sizeof(CombineItem) == 32, "CombineItem is 32 bytes");
+
+struct Plan {
+  std::vector<WorkItem> items;     // in launch order
+  std::vector<CombineItem> combine;
+  int64_t part_slots = 0;
+  // workspace layout (bytes)
+  size_t off_items = 0, off_combine = 0, off_ml = 0, off_acc = 0, total = 0;
+};
+
+ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
+                     const int32_t* bt_host, int32_t bt_stride, bool check_overlap);
+
+// Builds the plan for a device with num_cus compute units. The step must already be valid.
+void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, Plan& plan);
+
+void set_split_keys(int32_t prefill, int32_t decode);
+
+}  // namespace ppas

@@ -1,0 +1,151 @@
+"""Thin ctypes binding of libppas.so (C ABI in include/ppas.h).
+
+Argument marshalling only: every step of the computation runs in the library's
+HIP kernels. Device buffers are torch tensors (data pointers are passed through),
+descriptors and block-table host copies are NumPy int32 arrays. Importing this
+module fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libppas.so")
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_15171_amd.build`")
+_lib = ctypes.CDLL(LIB_PATH)
+
+PPAS_OK, PPAS_EINVAL, PPAS_ERANGE, PPAS_ENOSPACE, PPAS_EHIP, PPAS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("num_pages", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class PPASError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+_vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+_P = ctypes.POINTER(Shape)
+_lib.ppas_status_string.restype = ctypes.c_char_p
+_lib.ppas_status_string.argtypes = [ctypes.c_int]
+_lib.ppas_validate_step.restype = ctypes.c_int
+_lib.ppas_validate_step.argtypes = [_P, _vp, _i32, _vp, _i32]
+_lib.ppas_kv_append.restype = ctypes.c_int
+_lib.ppas_kv_append.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
+_lib.ppas_attn_workspace_bytes.restype = _sz
+_lib.ppas_attn_workspace_bytes.argtypes = [_P, _vp, _i32]
+_lib.ppas_attn_step.restype = ctypes.c_int
+_lib.ppas_attn_step.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]
+_lib.ppas_plan_items.restype = _i32
+_lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _i32, _vp, _i32]
+_lib.ppas_set_profile_events.restype = ctypes.c_int
+_lib.ppas_set_profile_events.argtypes = [_vp, _vp]
+_lib.ppas_set_split_keys.restype = ctypes.c_int
+_lib.ppas_set_split_keys.argtypes = [_i32, _i32]
+
+
+def status_string(status: int) -> str:
+    return _lib.ppas_status_string(int(status)).decode()
+
+
+def make_shape(n_q_heads: int = 16, n_kv_heads: int = 2, num_pages: int = 1, scale: float | None = None,
+               head_dim: int = 128, page_size: int = 16) -> Shape:
+    if scale is None:
+        scale = 1.0 / math.sqrt(head_dim)
+    return Shape(n_q_heads, n_kv_heads, head_dim, page_size, num_pages, scale)
+
+
+def _desc(desc) -> np.ndarray:
+    d = np.ascontiguousarray(desc, dtype=np.int32)
+    if d.ndim != 2 or d.shape[1] != 3:
+        raise ValueError("descriptors must be int32 [S, 3] (query_start, n_query, cached_len)")
+    return d
+
+
+def _host_ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _bt_host(bt_host):
+    return None if bt_host is None else np.ascontiguousarray(bt_host, dtype=np.int32)
+
+
+def _dev(t, name):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _check(st: int, what: str):
+    if st != PPAS_OK:
+        raise PPASError(st, what)
+
+
+def validate_step(shape: Shape, desc, bt_host=None, bt_stride: int | None = None) -> int:
+    d = _desc(desc)
+    bt = _bt_host(bt_host)
+    stride = bt_stride if bt_stride is not None else (bt.shape[1] if bt is not None else 1)
+    return _lib.ppas_validate_step(ctypes.byref(shape), _host_ptr(d), len(d), _host_ptr(bt), stride)
+
+
+def kv_append(shape: Shape, k_pages, v_pages, k_new, v_new, desc, bt_dev, bt_host=None, stream=None) -> None:
+    d = _desc(desc)
+    bt = _bt_host(bt_host)
+    st = _lib.ppas_kv_append(ctypes.byref(shape), _dev(k_pages, "k_pages"), _dev(v_pages, "v_pages"),
+                             _dev(k_new, "k_new"), _dev(v_new, "v_new"), _host_ptr(d), len(d),
+                             _dev(bt_dev, "block_table"), bt_dev.shape[1], _host_ptr(bt), _stream(stream))
+    _check(st, "ppas_kv_append")
+
+
+def attn_workspace_bytes(shape: Shape, desc) -> int:
+    d = _desc(desc)
+    return int(_lib.ppas_attn_workspace_bytes(ctypes.byref(shape), _host_ptr(d), len(d)))
+
+
+def attn_step(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, workspace, bt_host=None, stream=None) -> None:
+    d = _desc(desc)
+    bt = _bt_host(bt_host)
+    st = _lib.ppas_attn_step(ctypes.byref(shape), _dev(out, "out"), _dev(q, "q"), _dev(k_pages, "k_pages"),
+                             _dev(v_pages, "v_pages"), _host_ptr(d), len(d), _dev(bt_dev, "block_table"),
+                             bt_dev.shape[1], _host_ptr(bt), _dev(workspace, "workspace"),
+                             workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "ppas_attn_step")
+
+
+def plan_items(shape: Shape, desc, num_cus: int = 256) -> np.ndarray:
+    """The planned work list as int32 [n, 8]: kind, seq, kv_head, row0, pos0, npos, key_lo, key_hi."""
+    d = _desc(desc)
+    n = _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), num_cus, None, 0)
+    if n < 0:
+        raise PPASError(n, "ppas_plan_items")
+    out = np.zeros((max(n, 1), 8), dtype=np.int32)
+    _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), num_cus, out.ctypes.data, n)
+    return out[:n]
+
+
+def set_split_keys(prefill: int = 0, decode: int = 0) -> None:
+    _check(_lib.ppas_set_split_keys(int(prefill), int(decode)), "ppas_set_split_keys")
+
+
+def set_profile_events(start_event, stop_event) -> None:
+    """hipEvent_t handles (ints) recorded around the packed attention kernel, or (None, None)."""
+    _check(_lib.ppas_set_profile_events(start_event, stop_event), "ppas_set_profile_events")

@@ -1,0 +1,157 @@
+"""The C ABI on the CPU: the library loads, exports every declared entry point,
+validates step descriptions without touching a GPU, and plans work that covers
+every visible (row, head, key) triple exactly once."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_15171_amd import inputs as I
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ppas = pytest.importorskip("paper_2608_15171_amd.ppas", reason="libppas.so not built")
+
+
+def declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            txt = open(os.path.join(ROOT, "include", fn)).read()
+            txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+            names |= set(re.findall(r"\b(ppas_[a-z_0-9]+)\s*\(", txt))
+    return sorted(names)
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 7
+    lib = ctypes.CDLL(ppas.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4, -5):
+        assert ppas.status_string(st).startswith("PPAS_")
+    assert "unknown" in ppas.status_string(7)
+
+
+def shape(**kw):
+    base = dict(n_q_heads=16, n_kv_heads=2, num_pages=100)
+    base.update(kw)
+    return ppas.make_shape(**base)
+
+
+GOOD = np.array([[0, 1, 30], [1, 20, 5]], dtype=np.int32)
+BT = np.array([[0, 1, -1], [2, 3, -1]], dtype=np.int32)
+
+
+def test_validate_good_and_empty():
+    assert ppas.validate_step(shape(), GOOD, BT) == ppas.PPAS_OK
+    assert ppas.validate_step(shape(), np.zeros((0, 3), np.int32), None, 1) == ppas.PPAS_OK
+
+
+@pytest.mark.parametrize("desc,code", [
+    ([[0, 0, 30], [0, 20, 5]], "EINVAL"),          # n_query 0
+    ([[0, 1, -1], [1, 20, 5]], "EINVAL"),          # negative cached_len
+    ([[1, 1, 30], [2, 20, 5]], "EINVAL"),          # query_start not from 0
+    ([[0, 1, 30], [2, 20, 5]], "EINVAL"),          # gap between requests
+    ([[0, 1, 60], [1, 20, 5]], "EINVAL"),          # 61 tokens need 4 pages > stride 3
+])
+def test_validate_bad_descriptors(desc, code):
+    assert ppas.validate_step(shape(), np.array(desc, np.int32), BT) == getattr(ppas, "PPAS_" + code)
+
+
+def test_validate_shapes():
+    assert ppas.validate_step(shape(head_dim=64), GOOD, BT) == ppas.PPAS_EUNSUPPORTED
+    assert ppas.validate_step(shape(page_size=32), GOOD, BT) == ppas.PPAS_EUNSUPPORTED
+    assert ppas.validate_step(shape(n_q_heads=8), GOOD, BT) == ppas.PPAS_EUNSUPPORTED
+    assert ppas.validate_step(shape(n_q_heads=8, n_kv_heads=1), GOOD, BT) == ppas.PPAS_OK
+    assert ppas.validate_step(shape(n_q_heads=15), GOOD, BT) == ppas.PPAS_EINVAL
+    for sc in (0.0, -1.0, float("nan"), float("inf")):
+        assert ppas.validate_step(shape(scale=sc), GOOD, BT) == ppas.PPAS_EINVAL
+    assert ppas.validate_step(shape(num_pages=0), GOOD, BT) == ppas.PPAS_EINVAL
+
+
+def test_validate_block_table_range_and_overlap():
+    assert ppas.validate_step(shape(num_pages=3), GOOD, BT) == ppas.PPAS_ERANGE
+    bad = BT.copy()
+    bad[1, 0] = -1
+    assert ppas.validate_step(shape(), GOOD, bad) == ppas.PPAS_ERANGE
+    # request 0 writes position 30 -> (page 1, slot 14); request 1 writes 5..24 -> (page 2, 5..15), (page 1, 0..8)
+    ov = np.array([[0, 1, -1], [2, 1, -1]], np.int32)
+    assert ppas.validate_step(shape(), GOOD, ov) == ppas.PPAS_OK       # different slots of page 1
+    # request 0 at position 21 -> (page 1, slot 5); request 1 writes (page 1, slots 5..15): a clash
+    ov2 = np.array([[0, 1, -1], [1, 3, -1]], np.int32)
+    assert ppas.validate_step(shape(), np.array([[0, 1, 21], [1, 20, 5]], np.int32), ov2) == ppas.PPAS_EINVAL
+
+
+def test_calls_reject_bad_input_before_any_device_work():
+    import torch
+    sh = shape()
+    st = ppas._lib.ppas_attn_step(ctypes.byref(sh), None, None, None, None, GOOD.ctypes.data, 2, None, 3,
+                                  BT.ctypes.data, None, 0, None)
+    assert st == ppas.PPAS_EINVAL
+    bad = np.array([[0, 0, 1]], np.int32)
+    st = ppas._lib.ppas_kv_append(ctypes.byref(sh), 1, 1, 1, 1, bad.ctypes.data, 1, 1, 3, None, None)
+    assert st == ppas.PPAS_EINVAL
+    assert ppas.attn_workspace_bytes(sh, bad) == 0
+    assert ppas.attn_workspace_bytes(sh, GOOD) > 0
+
+
+def check_coverage(spec, items):
+    """Every (row, query head) sees keys 0..p split over items without gaps or overlaps,
+    and each item gives each of its rows at least one visible key."""
+    desc = spec.descriptors()
+    cover = {}
+    for kind, s, g, row0, pos0, npos, lo, hi in items.tolist():
+        qs, n, c = (int(x) for x in desc[s])
+        assert kind == (1 if n == 1 else 0)
+        assert qs <= row0 and row0 + npos <= qs + n and pos0 == c + (row0 - qs)
+        for r in range(npos):
+            p = pos0 + r
+            assert lo <= p, "an item with no visible key for one of its rows"
+            for h in range(g * 8, g * 8 + 8):
+                cover.setdefault((row0 + r, h), []).append((lo, min(hi, p + 1)))
+    assert len(cover) == spec.n_rows * spec.n_q_heads
+    for s in range(len(desc)):
+        qs, n, c = (int(x) for x in desc[s])
+        for i in range(n):
+            for h in range(spec.n_q_heads):
+                rng = sorted(cover[(qs + i, h)])
+                assert rng[0][0] == 0 and rng[-1][1] == c + i + 1
+                for a, b in zip(rng, rng[1:]):
+                    assert a[1] == b[0]
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("splits", [(0, 0), (64, 32), (128, 96)])
+def test_plan_covers_visible_keys_once(seed, splits):
+    spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
+    ppas.set_split_keys(*splits)
+    try:
+        items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
+    finally:
+        ppas.set_split_keys(0, 0)
+    check_coverage(spec, items)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_plan_covers_workloads(cfg):
+    spec = I.CONFIGS[cfg](0)
+    items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
+    if cfg in (1, 2):
+        check_coverage(spec, items)
+    # longest-first: the first launch slots hold the most keys on average
+    span = items[:, 7] - items[:, 6]
+    k = max(1, len(items) // 8)
+    assert span[:k].mean() >= span[-k:].mean()
+
+
+def test_plan_is_deterministic():
+    spec = I.config_high_pressure(0)
+    a = ppas.plan_items(shape(), spec.descriptors())
+    b = ppas.plan_items(shape(), spec.descriptors())
+    assert np.array_equal(a, b)

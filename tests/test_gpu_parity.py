@@ -1,0 +1,220 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Gates (stated for bf16 inputs with fp32 accumulation): over all compared output
+elements, max |gpu - oracle| <= 1e-2 and mean |gpu - oracle| <= 1e-3; page
+writes bit-exact. An extra internal gate bounds each row's relative L2 error by
+1e-2, which catches errors the absolute gate is too loose to see at long context.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle.attention as OA
+import oracle.kv_cache as OK
+from paper_2608_15171_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS, ROW_REL = 1e-2, 1e-3, 1e-2
+SENTINEL = 0xFFFF      # a NaN pattern in every pool slot no request owns
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_15171_amd import ppas, step
+    return ppas, step, torch
+
+
+def oracle_out(data, scale, rows=None):
+    return OA.step_attention_from_data(data, scale, rows=rows)
+
+
+def compare(gpu, ref, rows=None, label=""):
+    if rows is not None:
+        gpu, ref = gpu[rows], ref[rows]
+    assert np.isfinite(gpu).all(), f"{label}: non-finite output"
+    err = np.abs(gpu - ref)
+    mx, mean = float(err.max()), float(err.mean())
+    num = np.sqrt(((gpu - ref) ** 2).sum(axis=-1))
+    den = np.sqrt((ref ** 2).sum(axis=-1))
+    rel = float((num / np.maximum(den, 1e-30)).max())
+    print(f"{label}: max_abs={mx:.3e} mean_abs={mean:.3e} row_rel_max={rel:.3e}", flush=True)
+    assert mx <= MAX_ABS, f"{label}: max abs {mx}"
+    assert mean <= MEAN_ABS, f"{label}: mean abs {mean}"
+    assert rel <= ROW_REL, f"{label}: row relative L2 {rel}"
+
+
+def run_step(lib, spec, seed, permute=True, splits=(0, 0), pool_fill=SENTINEL, spare=5):
+    ppas, step, torch = lib
+    data = I.make_step_data(spec, seed)
+    bt, npages = I.make_block_table(spec, seed, permute=permute, spare_pages=spare)
+    ppas.set_split_keys(*splits)
+    try:
+        ds = step.DeviceStep(data, bt, npages, pool_fill=pool_fill)
+        ds.fill_history()
+        ds.run()
+        torch.cuda.synchronize()
+    finally:
+        ppas.set_split_keys(0, 0)
+    return data, ds
+
+
+# ------------------------------------------------------------------ kv_append
+
+@pytest.mark.parametrize("seed", range(6))
+def test_kv_append_bit_exact(lib, seed):
+    ppas, step, torch = lib
+    spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
+    print(f"kv_append seed={seed} seqs={[(s.n_query, s.cached_len) for s in spec.seqs]}", flush=True)
+    data = I.make_step_data(spec, seed, with_history=False)
+    bt, npages = I.make_block_table(spec, seed, spare_pages=4)
+    ds = step.DeviceStep(data, bt, npages, pool_fill=SENTINEL)
+    k0, v0 = step.bits_of(ds.k_pages), step.bits_of(ds.v_pages)
+    ds.append()
+    torch.cuda.synchronize()
+    kw, vw = OK.append(k0, v0, data.k_new, data.v_new, data.desc, bt, 16)
+    assert np.array_equal(step.bits_of(ds.k_pages), kw)
+    assert np.array_equal(step.bits_of(ds.v_pages), vw)
+
+
+def test_kv_append_history_round_trip(lib):
+    ppas, step, torch = lib
+    spec = I.config_small(0)
+    data = I.make_step_data(spec, 1)
+    bt, npages = I.make_block_table(spec, 1, spare_pages=3)
+    ds = step.DeviceStep(data, bt, npages, pool_fill=SENTINEL)
+    ds.fill_history()
+    ds.append()
+    torch.cuda.synchronize()
+    kp, vp = step.bits_of(ds.k_pages), step.bits_of(ds.v_pages)
+    for s in range(len(spec.seqs)):
+        qs, n, c = (int(x) for x in data.desc[s])
+        k, v = OK.gather(kp, vp, bt[s], c + n, 16)
+        assert np.array_equal(k, OA.logical_kv(data.k_hist[s], data.k_new[qs:qs + n]))
+        assert np.array_equal(v, OA.logical_kv(data.v_hist[s], data.v_new[qs:qs + n]))
+    # the spare pages were never written
+    used = set(bt[bt >= 0].tolist())
+    spare = [p for p in range(npages) if p not in used]
+    assert (kp[spare] == SENTINEL).all() and (vp[spare] == SENTINEL).all()
+
+
+# ------------------------------------------------------------------ attention, small
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("splits", [(0, 0), (64, 32), (192, 96)])
+def test_attention_fuzz(lib, seed, splits):
+    spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
+    print(f"fuzz seed={seed} splits={splits} seqs={[(s.n_query, s.cached_len) for s in spec.seqs]}", flush=True)
+    data, ds = run_step(lib, spec, seed, splits=splits)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"fuzz{seed}/{splits}")
+
+
+def test_attention_small_config(lib):
+    spec = I.config_small(0)
+    data, ds = run_step(lib, spec, 0)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label="512+4dec")
+
+
+def test_attention_small_config_split(lib):
+    spec = I.config_small(0)
+    data, ds = run_step(lib, spec, 0, splits=(128, 64))
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label="512+4dec split")
+
+
+def test_attention_edge_cases(lib):
+    # single-token prefill at 0, tiny chunks, chunk ending exactly on page/tile/block edges,
+    # decode at cached_len 0 (one key), ragged tails of 1 position
+    seqs = [I.Seq(1, 0, 0), I.Seq(2, 0, 1), I.Seq(17, 15, 2), I.Seq(16, 48, 3), I.Seq(64, 64, 4),
+            I.Seq(1, 63, 5), I.Seq(1, 64, 6), I.Seq(33, 1, 7), I.Seq(3, 127, 8)]
+    spec = I.StepSpec("edges", seqs)
+    for splits in [(0, 0), (64, 32)]:
+        data, ds = run_step(lib, spec, 21, splits=splits)
+        out = ds.out_f64()
+        compare(out, oracle_out(data, ds.shape.scale), label=f"edges{splits}")
+        # a row that sees one key returns that key's value exactly
+        v0 = OA.bf16_to_f64(data.v_new[0])
+        assert np.array_equal(out[0], np.repeat(v0, 8, axis=0))
+
+
+def test_tp_shard_shape(lib):
+    # one KV head with its 8 query heads: the shape of one tensor-parallel shard
+    spec = I.random_small_step(5, max_seqs=4, max_n=50, max_c=200, n_q_heads=8, n_kv_heads=1)
+    data, ds = run_step(lib, spec, 5)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label="tp-shard")
+
+
+def test_permuted_block_table_is_bit_identical(lib):
+    spec = I.random_small_step(3, max_seqs=6, max_n=70, max_c=300)
+    _, a = run_step(lib, spec, 3, permute=True)
+    _, b = run_step(lib, spec, 3, permute=False)
+    assert np.array_equal(a.out_f64(), b.out_f64())
+
+
+def test_deterministic_and_pool_contents_irrelevant(lib):
+    spec = I.config_small(0)
+    _, a = run_step(lib, spec, 2, pool_fill=SENTINEL)
+    _, b = run_step(lib, spec, 2, pool_fill=0)
+    ppas, step, torch = lib
+    o1 = a.out_f64()
+    a.attend()
+    torch.cuda.synchronize()
+    assert np.array_equal(o1, a.out_f64())
+    assert np.array_equal(o1, b.out_f64())
+
+
+def test_empty_step_is_a_no_op(lib):
+    ppas, step, torch = lib
+    sh = ppas.make_shape(num_pages=4)
+    ws = torch.zeros(256, dtype=torch.uint8, device="cuda")
+    bt = torch.zeros((1, 1), dtype=torch.int32, device="cuda")
+    x = torch.zeros(1, dtype=torch.bfloat16, device="cuda")
+    ppas.attn_step(sh, x, x, x, x, np.zeros((0, 3), np.int32), bt, ws)
+    ppas.kv_append(sh, x, x, x, x, np.zeros((0, 3), np.int32), bt)
+    torch.cuda.synchronize()
+
+
+def test_workspace_too_small_is_rejected(lib):
+    ppas, step, torch = lib
+    spec = I.config_small(0)
+    data = I.make_step_data(spec, 0)
+    bt, npages = I.make_block_table(spec, 0)
+    ppas.set_split_keys(64, 32)
+    try:
+        ds = step.DeviceStep(data, bt, npages)
+        small = ds.workspace[: ds.workspace.numel() // 2]
+        with pytest.raises(ppas.PPASError) as e:
+            ppas.attn_step(ds.shape, ds.out, ds.q, ds.k_pages, ds.v_pages, ds.desc, ds.bt, small, ds.bt_host)
+        assert e.value.status == ppas.PPAS_ENOSPACE
+    finally:
+        ppas.set_split_keys(0, 0)
+
+
+# ------------------------------------------------------------------ attention, full-size workloads
+
+def sample_rows(spec, g, per_seq=12):
+    rows = []
+    desc = spec.descriptors()
+    for s, (qs, n, c) in enumerate(desc.tolist()):
+        if n == 1:
+            rows.append(qs)
+            continue
+        cand = {0, 1, n - 1, n - 2, 15, 16, 63, 64, n // 2}
+        cand |= set(int(x) for x in g.integers(0, n, size=per_seq))
+        rows += [qs + i for i in sorted(cand) if 0 <= i < n]
+    return sorted(set(rows))
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_attention_full_size_sampled(lib, cfg):
+    ppas, step, torch = lib
+    spec = I.CONFIGS[cfg](0)
+    print(f"config {cfg} {spec.name}: rows={spec.n_rows}", flush=True)
+    data, ds = run_step(lib, spec, 0, spare=0)
+    rows = sample_rows(spec, I.rng(0, 77))
+    ref = oracle_out(data, ds.shape.scale, rows=rows)
+    out = ds.out_f64()
+    compare(out, ref, rows=rows, label=f"config{cfg} sampled {len(rows)} rows")
+    assert np.isfinite(out).all()
