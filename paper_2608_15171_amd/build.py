@@ -24,6 +24,8 @@ HIPCC_FLAGS = [
     "-fPIC",
     "-shared",
     "-Wall",
+    # code object v5 loads under both the system ROCm runtime and the one PyTorch bundles
+    "-mcode-object-version=5",
     # no packed-fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

@@ -16,7 +16,31 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libppas.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_15171_amd.build`")
+
+# PyTorch wheels carry their own HIP runtime. Import torch first so that the
+# library's libamdhip64.so.7 dependency binds to the runtime torch already
+# loaded (same SONAME): device pointers and streams are then shared by one HIP
+# runtime. Without torch, the system ROCm runtime is used.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    torch = None
 _lib = ctypes.CDLL(LIB_PATH)
+
+
+def _hip_runtimes() -> set:
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            path = line.split()[-1] if len(line.split()) >= 6 else ""
+            if os.path.basename(path).startswith("libamdhip64.so"):
+                paths.add(os.path.realpath(path))
+    return paths
+
+
+if len(_hip_runtimes()) > 1:
+    raise ImportError(f"two HIP runtimes are loaded in this process ({sorted(_hip_runtimes())}); "
+                      "import torch before loading libppas.so")
 
 PPAS_OK, PPAS_EINVAL, PPAS_ERANGE, PPAS_ENOSPACE, PPAS_EHIP, PPAS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 
