@@ -25,7 +25,9 @@ import os
 import sys
 import time
 
-WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4}
+WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
+             # diagnostics: parts of the pressure step alone
+             "pressure-decode": "pressure-decode", "pressure-prefill": "pressure-prefill"}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -123,7 +125,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    spec = I.CONFIGS[WORKLOADS[args.workload]](args.seed)
+    key = WORKLOADS[args.workload]
+    spec = (I.CONFIGS[key] if isinstance(key, int) else I.DIAGNOSTICS[key])(args.seed)
     data = I.make_step_data(spec, args.seed)
     bt, npages = I.make_block_table(spec, args.seed, permute=True)
     ds = DeviceStep(data, bt, npages)

@@ -28,8 +28,9 @@
  * Layouts
  *   q, out      [T][n_q_heads][128] bf16, row t = query token t of the step.
  *   k_new,v_new [T][n_kv_heads][128] bf16, the step's new keys/values, same rows.
- *   k_pages     [num_pages][n_kv_heads][16][128] bf16: per page and KV head,
- *               16 token rows of 128 contiguous features.
+ *   k_pages     [num_pages][n_kv_heads][16][16][8] bf16: per page and KV head,
+ *               16 chunks of 8 consecutive features; chunk c holds the 16
+ *               tokens' features 8c..8c+7, token after token (chunk-major).
  *   v_pages     [num_pages][n_kv_heads][128][16] bf16: per page and KV head,
  *               128 feature rows of 16 contiguous tokens.
  *   block_table [n_seqs][bt_stride] int32: entry j of request s is the physical
@@ -97,7 +98,7 @@ ppas_status ppas_validate_step(const ppas_shape* shape, const ppas_seq* seqs, in
  * processed tokens' keys and values are stored in the KV cache).
  * For every request s and i < n_query: position p = cached_len + i,
  * page = block_table[s][p / 16], slot = p % 16;
- *   k_pages[page][g][slot][:] = k_new[query_start + i][g][:]
+ *   k_pages[page][g][d / 8][slot][d % 8] = k_new[query_start + i][g][d]
  *   v_pages[page][g][:][slot] = v_new[query_start + i][g][:]   for every KV head g.
  * Bit-exact copies; no other byte of the pools is written. block_table_dev is
  * the device copy of the table; block_table_host (nullable) is a host copy used

@@ -8,8 +8,9 @@ page layout; the reading used throughout is:
 
   * page size P tokens; request s's logical page j (positions jP..jP+P-1) lives in
     physical page block_table[s, j];
-  * the K pool is [num_pages, Hkv, P, D]: within a page, one KV head's keys are
-    P rows of D contiguous elements (token-major);
+  * the K pool is [num_pages, Hkv, D/8, P, 8]: within a page, one KV head's keys
+    are split into D/8 chunks of 8 consecutive features, and each chunk holds
+    the P tokens' 8 features contiguously (chunk-major);
   * the V pool is [num_pages, Hkv, D, P]: within a page, one KV head's values are
     stored feature-major, P consecutive tokens per feature.
 
@@ -25,7 +26,7 @@ import numpy as np
 def append(k_pool, v_pool, k_new, v_new, desc, block_table, page_size: int):
     """Return copies of the pools with every request's new rows written.
 
-    k_pool: [num_pages, Hkv, P, D]; v_pool: [num_pages, Hkv, D, P]; k_new, v_new: [T, Hkv, D];
+    k_pool: [num_pages, Hkv, D/8, P, 8]; v_pool: [num_pages, Hkv, D, P]; k_new, v_new: [T, Hkv, D];
     desc: [S, 3] of (query_start, n_query, cached_len); block_table: [S, stride].
     """
     kp = np.array(k_pool, copy=True)
@@ -35,7 +36,8 @@ def append(k_pool, v_pool, k_new, v_new, desc, block_table, page_size: int):
         pos = c + np.arange(n)
         page = np.asarray(block_table)[s, pos // page_size]
         slot = pos % page_size
-        kp[page, :, slot, :] = k_new[qs:qs + n]
+        H, D = k_new.shape[1], k_new.shape[2]
+        kp[page, :, :, slot, :] = k_new[qs:qs + n].reshape(n, H, D // 8, 8)
         vp[page, :, :, slot] = v_new[qs:qs + n]
     return kp, vp
 
@@ -46,7 +48,8 @@ def gather(k_pool, v_pool, block_table_row, length: int, page_size: int):
     pos = np.arange(length)
     page = np.asarray(block_table_row)[pos // page_size]
     slot = pos % page_size
-    k = np.asarray(k_pool)[page, :, slot, :]
+    kc = np.asarray(k_pool)[page, :, :, slot, :]              # [length, Hkv, D/8, 8]
+    k = kc.reshape(length, kc.shape[1], -1)
     v = np.asarray(v_pool)[page, :, :, slot]
     return k, v
 
@@ -61,6 +64,7 @@ def fill_history(k_pool, v_pool, k_hist, v_hist, block_table, page_size: int):
         pos = np.arange(len(k_hist[s]))
         page = np.asarray(block_table)[s, pos // page_size]
         slot = pos % page_size
-        kp[page, :, slot, :] = k_hist[s]
+        L, H, D = k_hist[s].shape
+        kp[page, :, :, slot, :] = k_hist[s].reshape(L, H, D // 8, 8)
         vp[page, :, :, slot] = v_hist[s]
     return kp, vp

@@ -8,6 +8,9 @@
 // scale * q.k, applied to V; computed online over key blocks in the base-2
 // domain (running max m, running sum l, unnormalised accumulator), fp32
 // accumulation, probabilities rounded to bf16 for the PV product.
+//
+// Page layouts: K pages are chunk-major, [16 chunks of 8 features][16 slots][8];
+// V pages are feature-major, [128 features][16 slots].
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -17,10 +20,14 @@
 namespace ppas {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void global_cvoid;
 
 struct StepArgs {
   const uint16_t* q;
@@ -37,22 +44,56 @@ struct StepArgs {
 };
 
 constexpr int kThreads = 256;
-constexpr int kStageBytes = 32768;   // one 64-key block: 16 KB of K + 16 KB of V
+constexpr int kRegion = 1024;              // one wave's 64 x 16-byte LDS transfer
+constexpr int kBlockBytes = 16 * kRegion;  // K (or V) of one 64-key block
 constexpr float kNegInf = -__builtin_inff();
+constexpr int kPageElems = kPage * kHeadDim;
+constexpr int kChunkElems = kPage * 8;     // one 8-feature chunk of a K page
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-
+__device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// One v_cvt_pk_bf16_f32: two floats to a packed bf16 pair, nearest-even.
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return uint32_t(__builtin_bit_cast(uint16_t, (__bf16)a)) |
-         (uint32_t(__builtin_bit_cast(uint16_t, (__bf16)b)) << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __builtin_bit_cast(float, u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __builtin_bit_cast(float, u & 0xffff0000u); }
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// acc + lo + hi of a packed bf16 pair, exactly, in one dot instruction.
+__device__ __forceinline__ float sum_bf16x2(uint32_t pr, float acc) {
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pr), one, acc, false);
+}
+
+// 16 bytes from global memory into LDS: lane L of the wave lands at lds + 16 L.
+__device__ __forceinline__ void dma16(const uint16_t* g, char* lds) {
+  __builtin_amdgcn_global_load_lds((global_cvoid*)g, (lds_void*)lds, 16, 0, 0);
+}
+
+// Wait for this wave's outstanding global loads (including LDS transfers).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Online-softmax bookkeeping with a lazy maximum: a row's running max m (base-2
+// logits) is only raised when the block's max exceeds it by more than kSlack, so
+// the accumulator rescale is skipped on almost every block. Probabilities are
+// then bounded by 2^kSlack, which fp32 sums and bf16 operands hold exactly as
+// well as values <= 1. Exact: every term and the final sum share the same m.
+constexpr float kSlack = 8.f;
+template <int N, typename Acc>
+__device__ __forceinline__ void rescale_if_grown(float block_max, float& m_run, float& l_run, Acc (&acc)[N]) {
+  const bool grow = block_max > m_run + kSlack;
+  if (__any(grow)) {
+    const float m_new = grow ? block_max : m_run;
+    const float alpha = grow ? fast_exp2(m_run - m_new) : 1.f;
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int t = 0; t < N; ++t) acc[t] *= alpha;
+  }
+}
 
 // Zero the bf16 elements of an 8-element chunk whose index (first + e) is >= lim.
 __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
@@ -72,173 +113,247 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
 // a row). S^T = K Q^T and O^T += V^T P^T on 32x32x16 MFMAs, so every softmax
 // reduction stays inside a lane plus one exchange across the two half-waves.
 //
-// LDS per stage: K block [64 keys][128 d] with the 16-byte chunk index of key k
-// XOR-ed by (k & 15); V block [4 pages][128 d][16 keys] with the 16-byte half of
-// feature row d XOR-ed by bit 2 ^ bit 3 of d. Both keep MFMA operand reads free
-// of bank conflicts.
+// MFMA row m of a 32-key tile reads key pi(m), which swaps the middle two groups
+// of 4 in each 16, so that half-wave h ends up holding keys 16s+8h..16s+8h+7 of
+// the P^T operand of k-step s.
+//
+// LDS holds each 64-key block in MFMA operand order, written straight from
+// global memory by 16-byte LDS transfers: K region (t, j) = 8t + j holds, at
+// 16 L, lane L's A chunk for key tile t and k-step j (key 32t + pi(L & 31),
+// features 16j + 8(L >> 5) .. +7); V region (tt, s) = 4tt + s holds lane L's V^T
+// chunk (feature 32tt + (L & 31), keys 16s + 8(L >> 5) .. +7). Every operand
+// read is then base + 16 L + constant, free of bank conflicts, and each
+// transfer reads whole 32-byte runs of a page.
+//
+// Pipeline: iteration b issues the transfers of K(b+2) and V(b+1), runs the
+// QK^T MFMAs of block b+1 while it exponentiates block b, then the PV MFMAs of
+// block b while it reduces the max of block b+1. Blocks wholly below the tile's
+// first position need no mask and run the branch-free main loop; the last
+// blocks (diagonal, ragged tail) run the general iteration.
 // ---------------------------------------------------------------------------
+struct PrefillCtx {
+  const StepArgs* a;
+  const int32_t* btrow;
+  size_t head_off, page_stride;
+  int key_lo, kend, last_page;
+  int lane, w, n, h, pi_n;
+};
+
+struct PageIds {
+  int p[4];
+};
+
+__device__ __forceinline__ PageIds page_ids(const PrefillCtx& c, int blk) {
+  PageIds r;
+  const int first = (c.key_lo >> 4) + 4 * blk;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r.p[i] = c.btrow[min(first + i, c.last_page)];
+  return r;
+}
+
+// This wave's four K transfers of a block: regions 4w..4w+3, i.e. key tile w/2
+// and k-steps 4(w&1)..4(w&1)+3.
+__device__ __forceinline__ void dma_k(const PrefillCtx& c, const PageIds& pg, char* kbuf) {
+  // key tile w/2 spans pages 2(w/2) and 2(w/2)+1 of the block (explicit selects keep
+  // the page ids in registers)
+  const int lo = (c.w >> 1) ? pg.p[2] : pg.p[0];
+  const int hi = (c.w >> 1) ? pg.p[3] : pg.p[1];
+  const int page = (c.pi_n >> 4) ? hi : lo;
+  const uint16_t* base = c.a->kp + size_t(page) * c.page_stride + c.head_off + (c.pi_n & 15) * 8;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int j = 4 * (c.w & 1) + i;
+    dma16(base + (2 * j + c.h) * kChunkElems, kbuf + (4 * c.w + i) * kRegion);
+  }
+}
+
+// This wave's four V transfers of a block: regions 4w..4w+3, i.e. feature tile w
+// over the block's four pages.
+__device__ __forceinline__ void dma_v(const PrefillCtx& c, const PageIds& pg, char* vbuf) {
+  const size_t off = c.head_off + size_t(32 * c.w + c.n) * kPage + 8 * c.h;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    dma16(c.a->vp + size_t(pg.p[s]) * c.page_stride + off, vbuf + (4 * c.w + s) * kRegion);
+}
+
+__device__ __forceinline__ void qk_block(const char* kbuf, int lane, const bf16x8 (&qf)[8], f32x16 (&S)[2]) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) S[t][r] = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const u32x4 kv = lds16(kbuf + (8 * t + j) * kRegion + 16 * lane);
+      S[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[j], S[t], 0, 0, 0);
+    }
+}
+
+__device__ __forceinline__ float block_max(const f32x16 (&S)[2]) {
+  float mx = kNegInf;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[t][r]);
+  return fmaxf(mx, __shfl_xor(mx, 32));
+}
+
+// P^T operand of k-step s (keys 16s..16s+15) from tile s/2, registers 8(s%2)..;
+// returns the sum of the bf16-rounded probabilities (numerator and denominator
+// use the same weights).
+__device__ __forceinline__ float probs(const f32x16 (&S)[2], float scale_log2, float m_use, u32x4 (&pk)[4]) {
+  float lsum = 0.f;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x0 = fast_exp2(S[s >> 1][8 * (s & 1) + 2 * e] * scale_log2 - m_use);
+      const float x1 = fast_exp2(S[s >> 1][8 * (s & 1) + 2 * e + 1] * scale_log2 - m_use);
+      const uint32_t pr = pack_bf16x2(x0, x1);
+      pk[s][e] = pr;
+      lsum = sum_bf16x2(pr, lsum);
+    }
+  return lsum;
+}
+
+// O^T += V^T P^T. With the tail limit, keys >= kend contribute zero V (their
+// probabilities are already zero; this keeps unwritten slots out of the sum).
+template <bool kTail>
+__device__ __forceinline__ void pv_block(const char* vbuf, int lane, int h, const u32x4 (&pk)[4], f32x16 (&O)[4],
+                                         int kb, int kend) {
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      u32x4 vv = lds16(vbuf + (4 * tt + s) * kRegion + 16 * lane);
+      if (kTail) vv = keep_first(vv, 0, kend - (kb + 16 * s + 8 * h));
+      O[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), as_bf16x8(pk[s]), O[tt], 0, 0, 0);
+    }
+}
+
 __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& it, char* smem) {
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
-  const int n = lane & 31, h = lane >> 5;
+  PrefillCtx c;
+  c.a = &a;
+  c.lane = tid & 63;
+  c.w = tid >> 6;
+  c.n = c.lane & 31;
+  c.h = c.lane >> 5;
+  {
+    const int grp = (c.n >> 2) & 3;
+    const int base = (grp == 0) ? 0 : (grp == 1) ? 8 : (grp == 2) ? 4 : 12;
+    c.pi_n = (c.n & 16) | base | (c.n & 3);
+  }
+  c.btrow = a.bt + size_t(it.seq) * a.bt_stride;
+  c.head_off = size_t(it.kvh) * kPageElems;
+  c.page_stride = size_t(a.hkv) * kPageElems;
+  c.key_lo = it.key_lo;
+  c.kend = it.key_hi;
+  c.last_page = (it.key_hi - 1) >> 4;
+
   const int npos = it.npos_kind & 0xffff;
-  const int pl = 4 * w + (n >> 3);
-  const int hl = n & 7;
+  const int pl = 4 * c.w + (c.n >> 3);
+  const int hl = c.n & 7;
   const bool rvalid = pl < npos;
   const int p = it.pos0 + pl;
   const int qhead = it.kvh * kGroup + hl;
+  const float sl2 = a.scale_log2;
 
   // Q^T operand: k-step j covers features 16j..16j+15; this lane holds 8h..8h+7 of them.
   bf16x8 qf[8];
   {
-    const uint16_t* qrow = a.q + (size_t(it.row0 + (rvalid ? pl : 0)) * a.hq + qhead) * kHeadDim + 8 * h;
+    const uint16_t* qrow = a.q + (size_t(it.row0 + (rvalid ? pl : 0)) * a.hq + qhead) * kHeadDim + 8 * c.h;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      u32x4 v = rvalid ? ldg16(qrow + 16 * j) : u32x4{0, 0, 0, 0};
-      qf[j] = as_bf16x8(v);
-    }
+    for (int j = 0; j < 8; ++j) qf[j] = as_bf16x8(rvalid ? ldg16(qrow + 16 * j) : u32x4{0, 0, 0, 0});
   }
 
-  // MFMA row m of a 32-key tile reads key pi(m): swaps the middle two groups of 4
-  // in each 16 so that half-wave h ends up holding keys 16s+8h..16s+8h+7 of P^T.
-  int key_of_row[2];
-  {
-    const int grp = (n >> 2) & 3;
-    const int base = (grp == 0) ? 0 : (grp == 1) ? 8 : (grp == 2) ? 4 : 12;
-    const int km = (n & 16) | base | (n & 3);
-    key_of_row[0] = km;
-    key_of_row[1] = 32 + km;
-  }
+  // K buffers at smem + {0, 1} * kBlockBytes, V buffers after them
+  auto kbuf = [&](int i) { return smem + (i & 1) * kBlockBytes; };
+  auto vbuf = [&](int i) { return smem + (2 + (i & 1)) * kBlockBytes; };
+  const int nblk = (c.kend - c.key_lo + kPrefillBlock - 1) / kPrefillBlock;
+  // blocks 0..nfull-1 lie wholly at or below the tile's first position
+  const int nfull = min(nblk, (it.pos0 + 1 - c.key_lo) >> 6);
 
-  const int32_t* btrow = a.bt + size_t(it.seq) * a.bt_stride;
-  const size_t head_off = size_t(it.kvh) * kPage * kHeadDim;
-  const size_t page_stride = size_t(a.hkv) * kPage * kHeadDim;
-  const int kend = it.key_hi;
-  const int nblk = (kend - it.key_lo + kPrefillBlock - 1) / kPrefillBlock;
-
-  u32x4 sk[4], sv[4];
-  auto gload = [&](int kb) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key0 = kb + 16 * i;
-      if (key0 < kend) {
-        const size_t pg = size_t(btrow[key0 >> 4]) * page_stride + head_off;
-        sk[i] = ldg16(a.kp + pg + tid * 8);
-        sv[i] = ldg16(a.vp + pg + tid * 8);
-        const int lim = kend - key0;          // valid slots of this page
-        if (lim < 16) {
-          if ((tid >> 4) >= lim) sk[i] = u32x4{0, 0, 0, 0};
-          sv[i] = keep_first(sv[i], 8 * (tid & 1), lim);
-        }
-      } else {
-        sk[i] = u32x4{0, 0, 0, 0};
-        sv[i] = u32x4{0, 0, 0, 0};
-      }
-    }
-  };
-  auto swrite = [&](char* buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = 16 * i + (tid >> 4);
-      *reinterpret_cast<u32x4*>(buf + key * 256 + (((tid & 15) ^ (key & 15)) << 4)) = sk[i];
-      const int d = tid >> 1;
-      const int sw = ((d >> 2) ^ (d >> 3)) & 1;
-      *reinterpret_cast<u32x4*>(buf + 16384 + i * 4096 + d * 32 + (((tid & 1) ^ sw) << 4)) = sv[i];
-    }
-  };
-
-  f32x16 oacc[4];
+  f32x16 O[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[t][r] = 0.f;
+    for (int r = 0; r < 16; ++r) O[t][r] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
 
-  const int wave_pmin = it.pos0 + 4 * w;
-  const int wave_pmax = it.pos0 + min(4 * w + 3, npos - 1);
-
-  gload(it.key_lo);
-  swrite(smem);
+  // prologue: K(0), K(1), V(0) in flight; page ids of blocks 1 and 2 kept for the loop
+  const PageIds pg0 = page_ids(c, 0);
+  PageIds pg1 = page_ids(c, 1), pg2 = page_ids(c, 2);
+  dma_k(c, pg0, kbuf(0));
+  dma_k(c, pg1, kbuf(1));
+  dma_v(c, pg0, vbuf(0));
+  wait_vmem();
   __syncthreads();
 
-  for (int b = 0; b < nblk; ++b) {
-    char* cur = smem + (b & 1) * kStageBytes;
-    const int kb = it.key_lo + b * kPrefillBlock;
-    const bool has_next = b + 1 < nblk;
-    if (has_next) gload(kb + kPrefillBlock);
+  f32x16 SA[2], SB[2];
+  qk_block(kbuf(0), c.lane, qf, SA);
+  if (nfull >= 1) rescale_if_grown(block_max(SA) * sl2, m_run, l_run, O);
 
-    if (kb <= wave_pmax) {
-      // S^T = K Q^T: two 32-key tiles, 8 k-steps over the 128 features
-      f32x16 sacc[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const int key = key_of_row[t];
-          const u32x4 kv = *reinterpret_cast<const u32x4*>(cur + key * 256 + (((2 * j + h) ^ (key & 15)) << 4));
-          sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kv), qf[j], sacc[t], 0, 0, 0);
-        }
-      }
-      // causal mask: key (tile t, reg r) = kb + 32t + 16(r/8) + 8h + r%8, visible iff <= p
-      if (kb + kPrefillBlock - 1 > wave_pmin) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kb + 32 * t + 16 * (r >> 3) + 8 * h + (r & 7);
-            if (key > p) sacc[t][r] = kNegInf;
-          }
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[t][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx * a.scale_log2);
-      const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run - m_use);
-      m_run = m_new;
-
-      // P^T operand for k-step s (keys 16s..16s+15): tile s/2, registers 8(s%2)..8(s%2)+7
-      u32x4 pk[4];
-      float lsum = 0.f;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float x0 = fast_exp2(sacc[s >> 1][8 * (s & 1) + 2 * e] * a.scale_log2 - m_use);
-          const float x1 = fast_exp2(sacc[s >> 1][8 * (s & 1) + 2 * e + 1] * a.scale_log2 - m_use);
-          const uint32_t pr = pack_bf16x2(x0, x1);
-          pk[s][e] = pr;
-          lsum += bf16_lo(pr) + bf16_hi(pr);
-        }
-      }
-      l_run = l_run * alpha + lsum;
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[t][r] *= alpha;
-
-      // O^T += V^T P^T: 4 feature tiles of 32, 4 k-steps of 16 keys (one page each)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int d = 32 * t + n;
-        const int sw = ((d >> 2) ^ (d >> 3)) & 1;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const u32x4 vv = *reinterpret_cast<const u32x4*>(cur + 16384 + s * 4096 + d * 32 + ((h ^ sw) << 4));
-          oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), as_bf16x8(pk[s]), oacc[t], 0, 0, 0);
-        }
-      }
-    }
-
-    if (has_next) swrite(smem + ((b + 1) & 1) * kStageBytes);
+  // Main loop: blocks b and b + 1 both unmasked.
+  auto main_iter = [&](int b, f32x16 (&Scur)[2], f32x16 (&Snext)[2]) {
+    dma_k(c, pg2, kbuf(b));
+    dma_v(c, pg1, vbuf(b + 1));
+    pg1 = pg2;
+    pg2 = page_ids(c, b + 3);
+    const float m_use = (m_run == kNegInf) ? 0.f : m_run;
+    u32x4 pk[4];
+    qk_block(kbuf(b + 1), c.lane, qf, Snext);
+    l_run += probs(Scur, sl2, m_use, pk);
+    pv_block<false>(vbuf(b), c.lane, c.h, pk, O, 0, 0);
+    const float mx = block_max(Snext) * sl2;
+    wait_vmem();
     __syncthreads();
+    rescale_if_grown(mx, m_run, l_run, O);
+  };
+  int b = 0;
+  for (; b + 2 < nfull; b += 2) {
+    main_iter(b, SA, SB);
+    main_iter(b + 1, SB, SA);
+  }
+  if (b + 1 < nfull) {
+    main_iter(b, SA, SB);
+    ++b;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) SA[t] = SB[t];
+  }
+
+  // General iterations: the last unmasked block (its max is already folded in)
+  // and the blocks that need the causal mask or the ragged-tail limit.
+  for (; b < nblk; ++b) {
+    const int kb = c.key_lo + b * kPrefillBlock;
+    if (b >= nfull) {
+      // key (tile t, reg r) = kb + 32t + 16(r/8) + 8h + r%8, visible iff <= p
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kb + 32 * t + 16 * (r >> 3) + 8 * c.h + (r & 7);
+          if (key > p) SA[t][r] = kNegInf;
+        }
+      rescale_if_grown(block_max(SA) * sl2, m_run, l_run, O);
+    }
+    if (b + 2 < nblk) dma_k(c, pg2, kbuf(b));
+    if (b + 1 < nblk) dma_v(c, pg1, vbuf(b + 1));
+    pg1 = pg2;
+    pg2 = page_ids(c, b + 3);
+    const float m_use = (m_run == kNegInf) ? 0.f : m_run;
+    u32x4 pk[4];
+    if (b + 1 < nblk) qk_block(kbuf(b + 1), c.lane, qf, SB);
+    l_run += probs(SA, sl2, m_use, pk);
+    if (kb + kPrefillBlock > c.kend)
+      pv_block<true>(vbuf(b), c.lane, c.h, pk, O, kb, c.kend);
+    else
+      pv_block<false>(vbuf(b), c.lane, c.h, pk, O, kb, c.kend);
+    wait_vmem();
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 2; ++t) SA[t] = SB[t];
   }
 
   // Epilogue. O^T register r of feature tile t holds feature 32t + 8(r/4) + 4h + r%4.
@@ -251,24 +366,23 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = 32 * t + 8 * g + 4 * h;
+        const int d = 32 * t + 8 * g + 4 * c.h;
         u32x2 v;
-        v[0] = pack_bf16x2(oacc[t][4 * g] * inv, oacc[t][4 * g + 1] * inv);
-        v[1] = pack_bf16x2(oacc[t][4 * g + 2] * inv, oacc[t][4 * g + 3] * inv);
+        v[0] = pack_bf16x2(O[t][4 * g] * inv, O[t][4 * g + 1] * inv);
+        v[1] = pack_bf16x2(O[t][4 * g + 2] * inv, O[t][4 * g + 3] * inv);
         *reinterpret_cast<u32x2*>(orow + d) = v;
       }
   } else {
-    const int slot = it.part + 32 * w + n;
+    const int slot = it.part + 32 * c.w + c.n;
     float* acc = a.part_acc + size_t(slot) * kHeadDim;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = 32 * t + 8 * g + 4 * h;
-        *reinterpret_cast<f32x4*>(acc + d) =
-            f32x4{oacc[t][4 * g], oacc[t][4 * g + 1], oacc[t][4 * g + 2], oacc[t][4 * g + 3]};
+        const int d = 32 * t + 8 * g + 4 * c.h;
+        *reinterpret_cast<f32x4*>(acc + d) = f32x4{O[t][4 * g], O[t][4 * g + 1], O[t][4 * g + 2], O[t][4 * g + 3]};
       }
-    if (h == 0) a.part_ml[slot] = make_float2(m_run, l_tot);
+    if (c.h == 0) a.part_ml[slot] = make_float2(m_run, l_tot);
   }
 }
 
@@ -280,7 +394,9 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 // Lane (n = lane & 15, q = lane >> 4): K rows of tile t are keys 8*(m/4) + 4t + m%4,
 // so after S^T lane q holds keys 8q..8q+7 of the block, which is exactly the k
 // range of its P^T operand slot; its V^T operand is the 16 contiguous bytes of
-// feature d holding keys 8q..8q+7.
+// feature d holding keys 8q..8q+7. The QK^T reduction runs over features in the
+// order 32q + 8j + i (k-step j) for both the Q and K operands, so lane q's K
+// operand is chunks 4q..4q+3 of its key.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it, char* smem) {
   const int tid = threadIdx.x;
@@ -288,8 +404,6 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   const int n = lane & 15, q = lane >> 4;
   const bool hvalid = n < kGroup;
 
-  // Q^T operand: k-step j holds features 32q + 8j .. 32q + 8j + 7 (the same
-  // feature permutation is used for the K operand).
   bf16x8 qf[4];
   {
     const uint16_t* qrow = a.q + (size_t(it.row0) * a.hq + it.kvh * kGroup + (hvalid ? n : 0)) * kHeadDim + 32 * q;
@@ -298,40 +412,67 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   }
 
   const int32_t* btrow = a.bt + size_t(it.seq) * a.bt_stride;
-  const size_t head_off = size_t(it.kvh) * kPage * kHeadDim;
-  const size_t page_stride = size_t(a.hkv) * kPage * kHeadDim;
+  const size_t head_off = size_t(it.kvh) * kPageElems;
+  const size_t page_stride = size_t(a.hkv) * kPageElems;
   const int kend = it.key_hi;
   const int nblk = (kend - it.key_lo + kDecodeBlock - 1) / kDecodeBlock;
 
   const int krow = 8 * (n >> 2) + (n & 3);   // + 4t for tile t
 
-  u32x4 kr[2][4], vr[8];
-  auto gload = [&](int kb) {
+  // One 32-key block of this lane's MFMA operands: K rows for the two S^T tiles
+  // and V^T chunks for the eight feature tiles. Two sets alternate so that the
+  // next block's loads are in flight while the current one is consumed.
+  struct Blk {
+    u32x4 k[2][4];
+    u32x4 v[8];
+  };
+  auto k_src = [&](int key) {
+    return a.kp + size_t(btrow[key >> 4]) * page_stride + head_off + 4 * q * kChunkElems + (key & 15) * 8;
+  };
+  auto v_src = [&](int key0) {
+    return a.vp + size_t(btrow[key0 >> 4]) * page_stride + head_off + n * kPage + (key0 & 15);
+  };
+  // Full block: every key < kend.
+  auto gload = [&](Blk& B, int kb) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const uint16_t* src = k_src(kb + krow + 4 * t);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16(src + j * kChunkElems);
+    }
+    const uint16_t* src = v_src(kb + 8 * q);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) B.v[t] = ldg16(src + 16 * t * kPage);
+  };
+  // Ragged last block: keys >= kend load nothing and stay zero.
+  auto gload_tail = [&](Blk& B, int kb) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int key = kb + krow + 4 * t;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) B.k[t][j] = u32x4{0, 0, 0, 0};
       if (key < kend) {
-        const uint16_t* src = a.kp + size_t(btrow[key >> 4]) * page_stride + head_off + (key & 15) * kHeadDim + 32 * q;
+        const uint16_t* src = k_src(key);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kr[t][j] = ldg16(src + 8 * j);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) kr[t][j] = u32x4{0, 0, 0, 0};
+        for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16(src + j * kChunkElems);
       }
     }
     const int key0 = kb + 8 * q;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) B.v[t] = u32x4{0, 0, 0, 0};
     if (key0 < kend) {
-      const uint16_t* src = a.vp + size_t(btrow[key0 >> 4]) * page_stride + head_off + (key0 & 15) + n * kPage;
+      const uint16_t* src = v_src(key0);
       const int lim = kend - key0;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        vr[t] = ldg16(src + 16 * t * kPage);
-        if (lim < 8) vr[t] = keep_first(vr[t], 0, lim);
-      }
-    } else {
-#pragma unroll
-      for (int t = 0; t < 8; ++t) vr[t] = u32x4{0, 0, 0, 0};
+      for (int t = 0; t < 8; ++t) B.v[t] = keep_first(ldg16(src + 16 * t * kPage), 0, lim);
     }
+  };
+  auto load = [&](Blk& B, int blk) {
+    const int kb = it.key_lo + blk * kDecodeBlock;
+    if (kb + kDecodeBlock <= kend)
+      gload(B, kb);
+    else
+      gload_tail(B, kb);
   };
 
   f32x4 oacc[8];
@@ -339,26 +480,14 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   for (int t = 0; t < 8; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
 
-  int b = w;
-  if (b < nblk) gload(it.key_lo + b * kDecodeBlock);
-  for (; b < nblk; b += 4) {
-    const int kb = it.key_lo + b * kDecodeBlock;
-    u32x4 kc[2][4], vc[8];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kc[t][j] = kr[t][j];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) vc[t] = vr[t];
-    if (b + 4 < nblk) gload(kb + 4 * kDecodeBlock);
-
+  auto consume = [&](const Blk& B, int kb) {
     f32x4 sacc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kc[t][j]), qf[j], sacc[t], 0, 0, 0);
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[t][j]), qf[j], sacc[t], 0, 0, 0);
     }
     // S^T register r of tile t: key kb + 8q + 4t + r
     if (kb + kDecodeBlock > kend) {
@@ -375,10 +504,8 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[t][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * a.scale_log2);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
+    rescale_if_grown(mx * a.scale_log2, m_run, l_run, oacc);
+    const float m_use = (m_run == kNegInf) ? 0.f : m_run;
     u32x4 pb;
     float lsum = 0.f;
 #pragma unroll
@@ -388,14 +515,26 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
         const uint32_t pr = pack_bf16x2(fast_exp2(sacc[t][2 * e] * a.scale_log2 - m_use),
                                         fast_exp2(sacc[t][2 * e + 1] * a.scale_log2 - m_use));
         pb[2 * t + e] = pr;
-        lsum += bf16_lo(pr) + bf16_hi(pr);
+        lsum = sum_bf16x2(pr, lsum);
       }
-    l_run = l_run * alpha + lsum;
+    l_run += lsum;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      oacc[t] *= alpha;
-      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vc[t]), as_bf16x8(pb), oacc[t], 0, 0, 0);
-    }
+    for (int t = 0; t < 8; ++t)
+      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.v[t]), as_bf16x8(pb), oacc[t], 0, 0, 0);
+  };
+
+  // wave w takes blocks w, w+4, w+8, ...
+  Blk A, B;
+  int b = w;
+  if (b < nblk) load(A, b);
+  while (b < nblk) {
+    if (b + 4 < nblk) load(B, b + 4);
+    consume(A, it.key_lo + b * kDecodeBlock);
+    b += 4;
+    if (b >= nblk) break;
+    if (b + 4 < nblk) load(A, b + 4);
+    consume(B, it.key_lo + b * kDecodeBlock);
+    b += 4;
   }
 
   // Merge the four waves. O^T register r of feature tile t holds feature 16t + 4q + r.
@@ -443,7 +582,7 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
 }
 
 __global__ __launch_bounds__(kThreads, 2) void attn_step_kernel(StepArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStageBytes];
+  __shared__ __attribute__((aligned(1024))) char smem[4 * kBlockBytes];
   const WorkItem it = a.items[blockIdx.x];
   if ((it.npos_kind >> 16) == kKindDecode)
     decode_row(a, it, smem);
@@ -453,30 +592,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_step_kernel(StepArgs a) {
 
 // Merge split partials: for local row r of a combine item with partials
 // (m_s, l_s, acc_s), M = max m_s, out = sum 2^(m_s-M) acc_s / sum 2^(m_s-M) l_s.
-// One wave per row, two features per lane.
+// Block (item, y) handles rows 8y..8y+7 of the item; 32 lanes per row, 4
+// features per lane.
+constexpr int kCombineRowsPerBlock = 8;
 __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineItem* items, const float2* part_ml,
                                                            const float* part_acc, uint16_t* out, int hq) {
   const CombineItem ci = items[blockIdx.x];
   const int rows = ci.npos * kGroup;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int r = w; r < rows; r += kThreads / 64) {
-    float M = kNegInf;
-    for (int s = 0; s < ci.nsplit; ++s) M = fmaxf(M, part_ml[ci.part + s * rows + r].x);
-    const float M_use = (M == kNegInf) ? 0.f : M;
-    float L = 0.f, x0 = 0.f, x1 = 0.f;
-    for (int s = 0; s < ci.nsplit; ++s) {
-      const int slot = ci.part + s * rows + r;
-      const float2 ml = part_ml[slot];
-      const float f = fast_exp2(ml.x - M_use);
-      L += f * ml.y;
-      const float2 v = *reinterpret_cast<const float2*>(part_acc + size_t(slot) * kHeadDim + 2 * lane);
-      x0 += f * v.x;
-      x1 += f * v.y;
-    }
-    const float inv = 1.f / L;
-    uint16_t* orow = out + (size_t(ci.row0 + r / kGroup) * hq + ci.kvh * kGroup + r % kGroup) * kHeadDim;
-    *reinterpret_cast<uint32_t*>(orow + 2 * lane) = pack_bf16x2(x0 * inv, x1 * inv);
+  const int r = blockIdx.y * kCombineRowsPerBlock + (threadIdx.x >> 5);
+  if (r >= rows) return;
+  const int d0 = (threadIdx.x & 31) * 4;
+  float M = kNegInf;
+  for (int s = 0; s < ci.nsplit; ++s) M = fmaxf(M, part_ml[ci.part + s * rows + r].x);
+  const float M_use = (M == kNegInf) ? 0.f : M;
+  float L = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int s = 0; s < ci.nsplit; ++s) {
+    const int slot = ci.part + s * rows + r;
+    const float2 ml = part_ml[slot];
+    const float f = fast_exp2(ml.x - M_use);
+    L += f * ml.y;
+    acc += f * *reinterpret_cast<const f32x4*>(part_acc + size_t(slot) * kHeadDim + d0);
   }
+  const float inv = 1.f / L;
+  uint16_t* orow = out + (size_t(ci.row0 + r / kGroup) * hq + ci.kvh * kGroup + r % kGroup) * kHeadDim + d0;
+  u32x2 v;
+  v[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  v[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<u32x2*>(orow) = v;
 }
 
 hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp, const uint16_t* vp,
@@ -505,7 +649,8 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
     if (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess) return hipGetLastError();
   }
   if (n_comb > 0) {
-    hipLaunchKernelGGL(combine_kernel, dim3(n_comb), dim3(kThreads), 0, stream, comb, part_ml, part_acc, out, hq);
+    const int ymax = kTilePos * kGroup / kCombineRowsPerBlock;
+    hipLaunchKernelGGL(combine_kernel, dim3(n_comb, ymax), dim3(kThreads), 0, stream, comb, part_ml, part_acc, out, hq);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

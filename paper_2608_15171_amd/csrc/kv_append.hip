@@ -1,8 +1,9 @@
 // Scatter a step's new K/V rows into the paged cache (bit copies).
 //
 // One workgroup per (request, touched page, KV head). The K page of one head is
-// 16 token rows of 256 bytes: thread t copies the 16-byte chunk (slot t/16,
-// features 8(t%16)..) when that slot is one of the step's positions. The V page
+// 16 chunks of 8 features, each holding the 16 slots' 16-byte pieces: thread t
+// copies the piece (chunk t/16, slot t%16) when that slot is one of the step's
+// positions, so a workgroup's K stores are one contiguous 4 KB run. The V page
 // of one head is 128 feature rows of 16 tokens: thread t owns the chunk
 // (feature t/2, slots 8(t%2)..+7), gathers those slots from the new rows, and
 // stores the whole chunk when all 8 slots are new, else only the new elements.
@@ -40,13 +41,13 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
   const size_t base = (size_t(page) * a.hkv + g) * kPage * kHeadDim;
   const size_t row_stride = size_t(a.hkv) * kHeadDim;     // elements between new rows
 
-  // K: slot tid/16, features 8*(tid%16)..+7
+  // K: chunk tid/16 (features 8*(tid/16)..+7), slot tid%16
   {
-    const int slot = tid >> 4;
+    const int chunk = tid >> 4, slot = tid & 15;
     const int pos = pos_lo + slot;
     if (pos >= c && pos < c + nq) {
-      const uint16_t* src = a.kn + size_t(qs + pos - c) * row_stride + g * kHeadDim + 8 * (tid & 15);
-      *reinterpret_cast<u32x4*>(a.kp + base + slot * kHeadDim + 8 * (tid & 15)) = *reinterpret_cast<const u32x4*>(src);
+      const uint16_t* src = a.kn + size_t(qs + pos - c) * row_stride + g * kHeadDim + 8 * chunk;
+      *reinterpret_cast<u32x4*>(a.kp + base + 8 * tid) = *reinterpret_cast<const u32x4*>(src);
     }
   }
   // V: feature tid/2, slots 8*(tid%2)..+7

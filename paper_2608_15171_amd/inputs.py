@@ -119,11 +119,28 @@ def config_high_pressure(seed: int = 0) -> StepSpec:
     return StepSpec("pressure-2x1024+48dec", seqs, info={"prompt_lens": [int(x) for x in plen]})
 
 
+def config_pressure_decode_only(seed: int = 0) -> StepSpec:
+    """Diagnostic: only the 48 decode rows of the high-pressure step."""
+    full = config_high_pressure(seed)
+    return StepSpec("pressure-48dec-only", [s for s in full.seqs if s.n_query == 1])
+
+
+def config_pressure_prefill_only(seed: int = 0) -> StepSpec:
+    """Diagnostic: only the two 1,024-token chunks of the high-pressure step."""
+    full = config_high_pressure(seed)
+    return StepSpec("pressure-2x1024-only", [s for s in full.seqs if s.n_query > 1])
+
+
 CONFIGS = {
     1: config_small,
     2: config_small_budget,
     3: config_large_budget,
     4: config_high_pressure,
+}
+
+DIAGNOSTICS = {
+    "pressure-decode": config_pressure_decode_only,
+    "pressure-prefill": config_pressure_prefill_only,
 }
 
 

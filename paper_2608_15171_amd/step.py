@@ -38,7 +38,7 @@ class DeviceStep:
         self.bt = torch.from_numpy(self.bt_host).to(device)
         P, D, H = spec.page_size, spec.head_dim, spec.n_kv_heads
         fill = torch.tensor([pool_fill], dtype=torch.int32).to(torch.int16).item() if pool_fill else 0
-        self.k_pages = torch.full((num_pages, H, P, D), fill, dtype=torch.int16, device=device).view(torch.bfloat16)
+        self.k_pages = torch.full((num_pages, H, D // 8, P, 8), fill, dtype=torch.int16, device=device).view(torch.bfloat16)
         self.v_pages = torch.full((num_pages, H, D, P), fill, dtype=torch.int16, device=device).view(torch.bfloat16)
         self.out = torch.zeros((spec.n_rows, spec.n_q_heads, D), dtype=torch.bfloat16, device=device)
         ws = max(ppas.attn_workspace_bytes(self.shape, self.desc), 256)

@@ -18,13 +18,13 @@ def scalar_append(kp, vp, k_new, v_new, desc, bt, P):
             page, slot = int(bt[s][pos // P]), pos % P
             for g in range(k_new.shape[1]):
                 for d in range(k_new.shape[2]):
-                    kp[page, g, slot, d] = k_new[qs + i, g, d]
+                    kp[page, g, d // 8, slot, d % 8] = k_new[qs + i, g, d]
                     vp[page, g, d, slot] = v_new[qs + i, g, d]
     return kp, vp
 
 
 def pools(num_pages, Hkv, P, D, fill=0xFFFF):
-    return (np.full((num_pages, Hkv, P, D), fill, np.uint16), np.full((num_pages, Hkv, D, P), fill, np.uint16))
+    return (np.full((num_pages, Hkv, D // 8, P, 8), fill, np.uint16), np.full((num_pages, Hkv, D, P), fill, np.uint16))
 
 
 @pytest.mark.parametrize("seed", range(5))
@@ -41,16 +41,18 @@ def test_matches_scalar_loop(seed):
 
 def test_hand_worked_addresses():
     # one request, 14 cached tokens, 3 new: positions 14, 15, 16 with pages [7, 2]
-    # -> (page 7, slot 14), (page 7, slot 15), (page 2, slot 0)
-    P, D = 16, 2
+    # -> (page 7, slot 14), (page 7, slot 15), (page 2, slot 0); D = 16 features = 2 key chunks
+    P, D = 16, 16
     kp, vp = pools(8, 1, P, D)
-    k_new = np.array([[[1, 2]], [[3, 4]], [[5, 6]]], np.uint16)
+    k_new = np.arange(3 * D, dtype=np.uint16).reshape(3, 1, D)
     v_new = k_new + 100
     desc = np.array([[0, 3, 14]])
     bt = np.array([[7, 2]])
     ka, va = OK.append(kp, vp, k_new, v_new, desc, bt, P)
-    assert ka[7, 0, 14].tolist() == [1, 2] and ka[7, 0, 15].tolist() == [3, 4] and ka[2, 0, 0].tolist() == [5, 6]
-    assert va[7, 0, :, 14].tolist() == [101, 102] and va[2, 0, :, 0].tolist() == [105, 106]
+    # key feature d of a token sits in chunk d // 8, at offset d % 8 of that token's slot
+    assert ka[7, 0, 0, 14].tolist() == list(range(0, 8)) and ka[7, 0, 1, 14].tolist() == list(range(8, 16))
+    assert ka[7, 0, 0, 15].tolist() == list(range(16, 24)) and ka[2, 0, 1, 0].tolist() == list(range(40, 48))
+    assert va[7, 0, :, 14].tolist() == list(range(100, 116)) and va[2, 0, :, 0].tolist() == list(range(132, 148))
     changed = (ka != 0xFFFF).sum() + (va != 0xFFFF).sum()
     assert changed == 2 * 3 * D
 
