@@ -28,6 +28,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void global_cvoid;
+// The block table is read-only during a launch: reading it through the constant
+// address space lets uniform page-id loads use the scalar unit.
+typedef __attribute__((address_space(4))) const int32_t const_i32;
 
 struct StepArgs {
   const uint16_t* q;
@@ -133,10 +136,11 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
 // ---------------------------------------------------------------------------
 struct PrefillCtx {
   const StepArgs* a;
-  const int32_t* btrow;
-  size_t head_off, page_stride;
+  const_i32* btrow;
+  size_t page_stride;
   int key_lo, kend, last_page;
   int lane, w, n, h, pi_n;
+  uint32_t k_lane_off, v_lane_off;   // per-lane element offsets inside a page (head included)
 };
 
 struct PageIds {
@@ -152,28 +156,23 @@ __device__ __forceinline__ PageIds page_ids(const PrefillCtx& c, int blk) {
 }
 
 // This wave's four K transfers of a block: regions 4w..4w+3, i.e. key tile w/2
-// and k-steps 4(w&1)..4(w&1)+3.
+// (pages 2(w/2) and 2(w/2)+1 of the block) and k-steps 4(w&1)..4(w&1)+3.
 __device__ __forceinline__ void dma_k(const PrefillCtx& c, const PageIds& pg, char* kbuf) {
-  // key tile w/2 spans pages 2(w/2) and 2(w/2)+1 of the block (explicit selects keep
-  // the page ids in registers)
   const int lo = (c.w >> 1) ? pg.p[2] : pg.p[0];
   const int hi = (c.w >> 1) ? pg.p[3] : pg.p[1];
-  const int page = (c.pi_n >> 4) ? hi : lo;
-  const uint16_t* base = c.a->kp + size_t(page) * c.page_stride + c.head_off + (c.pi_n & 15) * 8;
+  const uint16_t* lo_base = c.a->kp + size_t(lo) * c.page_stride;
+  const uint16_t* hi_base = c.a->kp + size_t(hi) * c.page_stride;
+  const uint16_t* base = ((c.pi_n >> 4) ? hi_base : lo_base) + c.k_lane_off;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int j = 4 * (c.w & 1) + i;
-    dma16(base + (2 * j + c.h) * kChunkElems, kbuf + (4 * c.w + i) * kRegion);
-  }
+  for (int i = 0; i < 4; ++i) dma16(base + 2 * i * kChunkElems, kbuf + (4 * c.w + i) * kRegion);
 }
 
 // This wave's four V transfers of a block: regions 4w..4w+3, i.e. feature tile w
 // over the block's four pages.
 __device__ __forceinline__ void dma_v(const PrefillCtx& c, const PageIds& pg, char* vbuf) {
-  const size_t off = c.head_off + size_t(32 * c.w + c.n) * kPage + 8 * c.h;
 #pragma unroll
   for (int s = 0; s < 4; ++s)
-    dma16(c.a->vp + size_t(pg.p[s]) * c.page_stride + off, vbuf + (4 * c.w + s) * kRegion);
+    dma16(c.a->vp + size_t(pg.p[s]) * c.page_stride + c.v_lane_off, vbuf + (4 * c.w + s) * kRegion);
 }
 
 __device__ __forceinline__ void qk_block(const char* kbuf, int lane, const bf16x8 (&qf)[8], f32x16 (&S)[2]) {
@@ -232,6 +231,27 @@ __device__ __forceinline__ void pv_block(const char* vbuf, int lane, int h, cons
     }
 }
 
+// Instruction order for one main-loop iteration (scheduler hints only; they do
+// not change results): the K reads run a few MFMAs ahead, each QK^T MFMA of
+// block b+1 is followed by a share of block b's exponentials, and the PV MFMAs
+// of block b are interspersed with the max reduction of block b+1.
+constexpr int kSchedDs = 0x100, kSchedMfma = 0x008, kSchedValu = 0x002;
+__device__ __forceinline__ void interleave_main_iter() {
+  __builtin_amdgcn_sched_group_barrier(kSchedDs, 4, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSchedDs, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSchedDs, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 0);
+  }
+}
+
 __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& it, char* smem) {
   const int tid = threadIdx.x;
   PrefillCtx c;
@@ -245,9 +265,15 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
     const int base = (grp == 0) ? 0 : (grp == 1) ? 8 : (grp == 2) ? 4 : 12;
     c.pi_n = (c.n & 16) | base | (c.n & 3);
   }
-  c.btrow = a.bt + size_t(it.seq) * a.bt_stride;
-  c.head_off = size_t(it.kvh) * kPageElems;
+  c.btrow = (const_i32*)(a.bt) + size_t(it.seq) * a.bt_stride;
   c.page_stride = size_t(a.hkv) * kPageElems;
+  {
+    const uint32_t head_off = uint32_t(it.kvh) * kPageElems;
+    // K: chunk 2j + h of k-step j = 4(w&1) + i, slot pi(n) & 15
+    c.k_lane_off = head_off + (8 * (c.w & 1) + c.h) * kChunkElems + (c.pi_n & 15) * 8;
+    // V: feature 32w + n, slots 8h..8h+7
+    c.v_lane_off = head_off + (32 * c.w + c.n) * kPage + 8 * c.h;
+  }
   c.key_lo = it.key_lo;
   c.kend = it.key_hi;
   c.last_page = (it.key_hi - 1) >> 4;
@@ -307,6 +333,7 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
     l_run += probs(Scur, sl2, m_use, pk);
     pv_block<false>(vbuf(b), c.lane, c.h, pk, O, 0, 0);
     const float mx = block_max(Snext) * sl2;
+    interleave_main_iter();
     wait_vmem();
     __syncthreads();
     rescale_if_grown(mx, m_run, l_run, O);

@@ -13,6 +13,16 @@ std::atomic<int32_t> g_prefill_split{0};
 std::atomic<int32_t> g_decode_split{0};
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// decode cost / prefill cost above which the two kinds are interleaved
+#ifndef PPAS_INTERLEAVE_RATIO
+#define PPAS_INTERLEAVE_RATIO 0.5
+#endif
+constexpr double kInterleaveRatio = PPAS_INTERLEAVE_RATIO;
+// prefill items aimed at per compute unit when tiles need key splits
+#ifndef PPAS_PREFILL_ITEMS_PER_CU
+#define PPAS_PREFILL_ITEMS_PER_CU 2
+#endif
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 }  // namespace
 
@@ -102,7 +112,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
 
   int64_t ksp = g_prefill_split.load();
   if (ksp <= 0) {
-    const int64_t target = int64_t(4) * num_cus;
+    const int64_t target = int64_t(PPAS_PREFILL_ITEMS_PER_CU) * num_cus;
     ksp = std::max<int64_t>(1024, ceil_div(prefill_keys, target));
   }
   ksp = std::max<int64_t>(kPrefillBlock, ceil_div(ksp, kPrefillBlock) * kPrefillBlock);
@@ -153,15 +163,43 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
     }
   }
 
-  // Longest first, in cost buckets of 256 keys; inside a bucket keep items of the
-  // same request and KV head together so neighbours share keys in one L2.
-  std::stable_sort(jobs.begin(), jobs.end(), [](const Job& a, const Job& b) {
+  // Longest first within each kind, in cost buckets of 256 keys; inside a bucket
+  // keep items of the same request and KV head together so neighbours share keys
+  // in one L2.
+  auto lpt = [](const Job& a, const Job& b) {
     const int64_t ca = int64_t(a.cost) >> 8, cb = int64_t(b.cost) >> 8;
     if (ca != cb) return ca > cb;
     for (int i = 0; i < 4; ++i)
       if (a.order_key[i] != b.order_key[i]) return a.order_key[i] < b.order_key[i];
     return false;
-  });
+  };
+  std::vector<Job> pre, dec;
+  for (const Job& j : jobs) ((j.item.npos_kind >> 16) == kKindDecode ? dec : pre).push_back(j);
+  std::stable_sort(pre.begin(), pre.end(), lpt);
+  std::stable_sort(dec.begin(), dec.end(), lpt);
+  // Prefill tiles load the matrix cores and decode items the memory system. When
+  // the decode work is comparable to the prefill work, they run best side by
+  // side: merge the two queues so that both advance at the same fraction of
+  // their total work and finish together. When decode is a small share, it goes
+  // last and fills the tail of the prefill rounds.
+  double tot_p = 0, tot_d = 0;
+  for (const Job& j : pre) tot_p += j.cost;
+  for (const Job& j : dec) tot_d += j.cost;
+  const bool interleave = tot_d >= kInterleaveRatio * tot_p;
+  jobs.clear();
+  size_t ip = 0, id = 0;
+  double done_p = 0, done_d = 0;
+  while (ip < pre.size() || id < dec.size()) {
+    const bool take_p = id >= dec.size() ||
+                        (ip < pre.size() && (!interleave || done_p * tot_d <= done_d * tot_p));
+    if (take_p) {
+      done_p += pre[ip].cost;
+      jobs.push_back(pre[ip++]);
+    } else {
+      done_d += dec[id].cost;
+      jobs.push_back(dec[id++]);
+    }
+  }
 
   // Workgroup b of a launch runs on XCD b % 8. Hand each XCD runs of 8
   // consecutive items of the sorted list, with runs dealt round-robin so every XCD
