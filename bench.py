@@ -33,6 +33,28 @@ PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
 
 
+KERNEL_SOURCES = ["paper_2608_15171_amd/csrc/attn_step.hip", "paper_2608_15171_amd/csrc/plan.cpp",
+                  "paper_2608_15171_amd/csrc/plan.h"]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the attention kernel from the committed rocprofv3 byte
+    counters (calibrated against a plain copy), or None when no record exists or the
+    kernel sources changed since the counters were taken."""
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", f"attn_step_kernel.{workload}.traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for src in KERNEL_SOURCES:
+        h.update(open(os.path.join(root, src), "rb").read())
+    if rec.get("kernel_sources_sha256") != h.hexdigest():
+        return None
+    return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
+
+
 class HipEvents:
     """hipEvent_t pairs through the HIP runtime (timing events on the launch stream)."""
 
@@ -205,7 +227,7 @@ def main():
         },
         "roofline": {
             "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "frac": round(achieved / peak, 4), "traffic": measured_traffic(args.workload),
             "kernel": "attn_step_kernel", "kernel_us": round(k_ms * 1e3, 2),
             "per_launch": {"flop": F, "bytes": B},
         },
