@@ -231,27 +231,6 @@ __device__ __forceinline__ void pv_block(const char* vbuf, int lane, int h, cons
     }
 }
 
-// Instruction order for one main-loop iteration (scheduler hints only; they do
-// not change results): the K reads run a few MFMAs ahead, each QK^T MFMA of
-// block b+1 is followed by a share of block b's exponentials, and the PV MFMAs
-// of block b are interspersed with the max reduction of block b+1.
-constexpr int kSchedDs = 0x100, kSchedMfma = 0x008, kSchedValu = 0x002;
-__device__ __forceinline__ void interleave_main_iter() {
-  __builtin_amdgcn_sched_group_barrier(kSchedDs, 4, 0);
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kSchedDs, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kSchedValu, 6, 0);
-  }
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kSchedDs, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 0);
-  }
-}
-
 __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& it, char* smem) {
   const int tid = threadIdx.x;
   PrefillCtx c;
@@ -333,7 +312,6 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
     l_run += probs(Scur, sl2, m_use, pk);
     pv_block<false>(vbuf(b), c.lane, c.h, pk, O, 0, 0);
     const float mx = block_max(Snext) * sl2;
-    interleave_main_iter();
     wait_vmem();
     __syncthreads();
     rescale_if_grown(mx, m_run, l_run, O);
