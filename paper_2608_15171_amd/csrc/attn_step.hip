@@ -54,6 +54,10 @@ constexpr int kPageElems = kPage * kHeadDim;
 constexpr int kChunkElems = kPage * 8;     // one 8-feature chunk of a K page
 
 __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+// Streaming load that bypasses cache retention (decode K/V are read exactly once).
+__device__ __forceinline__ u32x4 ldg16_nt(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -222,9 +226,9 @@ template <bool kTail>
 __device__ __forceinline__ void pv_block(const char* vbuf, int lane, int h, const u32x4 (&pk)[4], f32x16 (&O)[4],
                                          int kb, int kend) {
 #pragma unroll
-  for (int tt = 0; tt < 4; ++tt)
+  for (int s = 0; s < 4; ++s)
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int tt = 0; tt < 4; ++tt) {   // four independent accumulators in turn
       u32x4 vv = lds16(vbuf + (4 * tt + s) * kRegion + 16 * lane);
       if (kTail) vv = keep_first(vv, 0, kend - (kb + 16 * s + 8 * h));
       O[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vv), as_bf16x8(pk[s]), O[tt], 0, 0, 0);
@@ -443,11 +447,11 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     for (int t = 0; t < 2; ++t) {
       const uint16_t* src = k_src(kb + krow + 4 * t);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16(src + j * kChunkElems);
+      for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
     }
     const uint16_t* src = v_src(kb + 8 * q);
 #pragma unroll
-    for (int t = 0; t < 8; ++t) B.v[t] = ldg16(src + 16 * t * kPage);
+    for (int t = 0; t < 8; ++t) B.v[t] = ldg16_nt(src + 16 * t * kPage);
   };
   // Ragged last block: keys >= kend load nothing and stay zero.
   auto gload_tail = [&](Blk& B, int kb) {
@@ -459,7 +463,7 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       if (key < kend) {
         const uint16_t* src = k_src(key);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16(src + j * kChunkElems);
+        for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
       }
     }
     const int key0 = kb + 8 * q;

@@ -19,6 +19,10 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 #define PPAS_INTERLEAVE_RATIO 0.5
 #endif
 constexpr double kInterleaveRatio = PPAS_INTERLEAVE_RATIO;
+// when interleaving, prefill advances at this multiple of the decode fraction
+#ifndef PPAS_INTERLEAVE_BIAS
+#define PPAS_INTERLEAVE_BIAS 1.0
+#endif
 // prefill items aimed at per compute unit when tiles need key splits
 #ifndef PPAS_PREFILL_ITEMS_PER_CU
 #define PPAS_PREFILL_ITEMS_PER_CU 2
@@ -191,7 +195,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   double done_p = 0, done_d = 0;
   while (ip < pre.size() || id < dec.size()) {
     const bool take_p = id >= dec.size() ||
-                        (ip < pre.size() && (!interleave || done_p * tot_d <= done_d * tot_p));
+                        (ip < pre.size() && (!interleave || done_p * tot_d <= PPAS_INTERLEAVE_BIAS * done_d * tot_p));
     if (take_p) {
       done_p += pre[ip].cost;
       jobs.push_back(pre[ip++]);
