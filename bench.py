@@ -27,7 +27,9 @@ import time
 
 WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              # diagnostics: parts of the pressure step alone
-             "pressure-decode": "pressure-decode", "pressure-prefill": "pressure-prefill"}
+             "pressure-decode": "pressure-decode", "pressure-prefill": "pressure-prefill",
+             # 36-layer P-PAS serving trace (64 requests)
+             "trace": None}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -122,6 +124,59 @@ def cpu_baseline(data, scale, budget_s: float):
                       f"{frac:.2%} of each prefill chunk), all 16 heads, fp64 NumPy; {f:.3e} FLOP in {dt:.1f} s"}
 
 
+def run_trace_workload(args):
+    """The 36-layer serving trace: total attention time over every step and layer."""
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import trace_run as TR
+
+    setup = TR.make_setup(args.seed, mode=args.trace_mode, mbt=args.trace_mbt, layers=args.layers)
+    banks = TR.make_banks(args.seed, setup.bank_rows)
+    big = max(range(len(setup.steps)), key=lambda i: setup.steps[i].spec.n_rows)
+    print(f"trace: {len(setup.steps)} steps x {args.layers} layers, {len(setup.requests)} requests",
+          file=sys.stderr, flush=True)
+    res = TR.run(setup, banks, args.layers,
+                 progress=lambda i, n: print(f"step {i}/{n}", file=sys.stderr, flush=True))
+    t_attn = res["attn_ms_total"] * 1e-3
+    rec = {
+        "metric": METRIC,
+        "value": round(res["flops"] / t_attn / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": len(setup.steps),
+        "warmup": 0,
+        "ms_per_step": round(res["wall_ms"] / len(setup.steps), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"trace-{len(setup.requests)}req-{args.layers}layers-{args.trace_mode}"
+                               + ("" if args.trace_mode == "ppas" else f"{args.trace_mbt}"),
+                   "layers": args.layers, "requests": len(setup.requests), "scheduler_steps": len(setup.steps),
+                   "prefill_tokens": int(sum(s.prefill_tokens for s in setup.steps)),
+                   "decode_rows": int(sum(s.decode_rows for s in setup.steps)),
+                   "heads": "16q/2kv", "head_dim": 128, "page_size": 16},
+        "trace": {"attention_ms_total": round(res["attn_ms_total"], 3),
+                  "kv_append_ms_total": round(res["kv_append_ms_total"], 3),
+                  "wall_ms": round(res["wall_ms"], 1), "attn_launches": res["launches"],
+                  "flop_total": res["flops"], "decode_kv_bytes_total": res["decode_kv_bytes"],
+                  "roofline_ms": round(max(res["flops"] / (PEAK_TFLOPS * 1e12),
+                                           res["decode_kv_bytes"] / (PEAK_GBPS * 1e9)) * 1e3, 3),
+                  "largest_step_rows": setup.steps[big].spec.n_rows},
+        "roofline": {"bound": "mfma", "achieved": round(res["flops"] / t_attn / 1e12, 2), "peak": PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(res["flops"] / t_attn / 1e12 / PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": "attn_step_kernel"},
+    }
+    if not args.no_cpu_baseline:
+        data = TR.oracle_inputs(setup, banks, big, 0)
+        cb = cpu_baseline(data, 1.0 / math.sqrt(128.0), args.cpu_seconds)
+        cb["sample"] = "largest step of the trace, layer 0: " + cb["sample"]
+        rec["cpu_baseline"] = cb
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +186,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=36, help="trace workload: layers")
+    ap.add_argument("--trace-mode", choices=["ppas", "fixed"], default="ppas", help="trace workload: budget policy")
+    ap.add_argument("--trace-mbt", type=int, default=16384, help="trace workload: global token budget")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
@@ -147,6 +205,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.workload == "trace":
+        return run_trace_workload(args)
     key = WORKLOADS[args.workload]
     spec = (I.CONFIGS[key] if isinstance(key, int) else I.DIAGNOSTICS[key])(args.seed)
     data = I.make_step_data(spec, args.seed)

@@ -218,3 +218,24 @@ def test_attention_full_size_sampled(lib, cfg):
     out = ds.out_f64()
     compare(out, ref, rows=rows, label=f"config{cfg} sampled {len(rows)} rows")
     assert np.isfinite(out).all()
+
+
+# ------------------------------------------------------------------ serving trace
+
+def test_trace_steps_match_oracle(lib):
+    """A small P-PAS trace (small budgets, so prompts are chunked and pressure caps apply)
+    through persistent per-layer pools; sampled steps in every layer against the oracle."""
+    from paper_2608_15171_amd import trace_run as TR
+    setup = TR.make_setup(3, n_bursts=3, burst_size=3, mean_gap=6, prompt_range=(150, 600),
+                          output_range=(2, 6), layers=2, b_max=512, b_cap=128)
+    banks = TR.make_banks(3, setup.bank_rows)
+    n = len(setup.steps)
+    assert any(s.prefill_budget == 128 for s in setup.steps) and any(len(s.spec.seqs) > 2 for s in setup.steps)
+    picks = sorted({0, n // 3, n // 2, n - 1, max(range(n), key=lambda i: setup.steps[i].spec.n_rows),
+                    max(range(n), key=lambda i: len(setup.steps[i].spec.seqs))})
+    check = [(i, l) for i in picks for l in (0, 1)]
+    print(f"trace steps={n} checks={check}", flush=True)
+    res = TR.run(setup, banks, 2, check=check)
+    for (i, l), out in res["checks"].items():
+        data = TR.oracle_inputs(setup, banks, i, l)
+        compare(out.astype(np.float64), oracle_out(data, 1.0 / math.sqrt(128.0)), label=f"trace step {i} layer {l}")
