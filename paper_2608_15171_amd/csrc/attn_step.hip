@@ -409,7 +409,8 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it, char* smem) {
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
+  // the wave index is uniform; saying so keeps per-wave control flow scalar
+  const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, q = lane >> 4;
   const bool hvalid = n < kGroup;
 
@@ -425,8 +426,27 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   const size_t page_stride = size_t(a.hkv) * kPageElems;
   const int kend = it.key_hi;
   const int nblk = (kend - it.key_lo + kDecodeBlock - 1) / kDecodeBlock;
+  const int nmine = nblk > w ? (nblk - w + 3) / 4 : 0;   // blocks w, w+4, ... of this wave
 
-  const int krow = 8 * (n >> 2) + (n & 3);   // + 4t for tile t
+  const int krow = 8 * (n >> 2) + (n & 3);   // + 4t for tile t: key row of the K operand
+
+  // Page ids. Item key ranges start on 32-key boundaries, so block b covers
+  // pages first + 2b and first + 2b + 1. This wave's i-th block is b = w + 4i;
+  // lane L of a page-id register holds page 2(w + 4(i0 + L/2)) + (L & 1) for the
+  // register's base block i0, so one register serves 32 blocks and the ids of a
+  // block come out with two lane reads, with no load on the loop's critical path.
+  const int first_page = it.key_lo >> 4;
+  const int last_page = (kend - 1) >> 4;
+  auto load_pids = [&](int i0) {
+    const int blk = w + 4 * (i0 + (lane >> 1));
+    return btrow[min(first_page + 2 * blk + (lane & 1), last_page)];
+  };
+  // The planner caps decode key ranges at kDecodeMaxKeys, so a wave has at most 64 blocks.
+  static_assert(kDecodeMaxKeys <= 4 * 64 * kDecodeBlock, "two page-id registers per wave");
+  const int pid_lo = load_pids(0), pid_hi = load_pids(32);
+  // Complete the page-id loads here, once (the Q loads stay in flight), so the
+  // loop never waits on them.
+  asm volatile("" ::"v"(pid_lo), "v"(pid_hi));
 
   // One 32-key block of this lane's MFMA operands: K rows for the two S^T tiles
   // and V^T chunks for the eight feature tiles. Two sets alternate so that the
@@ -435,33 +455,44 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     u32x4 k[2][4];
     u32x4 v[8];
   };
-  auto k_src = [&](int key) {
-    return a.kp + size_t(btrow[key >> 4]) * page_stride + head_off + 4 * q * kChunkElems + (key & 15) * 8;
-  };
-  auto v_src = [&](int key0) {
-    return a.vp + size_t(btrow[key0 >> 4]) * page_stride + head_off + n * kPage + (key0 & 15);
+  // K row keys krow + 4t lie in the block's second page iff n >= 8; V chunk keys
+  // 8q..8q+7 iff q >= 2.
+  const uint32_t k_lane = uint32_t(head_off) + 4 * q * kChunkElems;
+  const uint32_t v_lane = uint32_t(head_off) + n * kPage + 8 * (q & 1);
+  auto bases = [&](int i, const uint16_t*& kbase, const uint16_t*& vbase) {
+    const int l0 = __builtin_amdgcn_readlane(pid_lo, 2 * (i & 31));
+    const int l1 = __builtin_amdgcn_readlane(pid_lo, 2 * (i & 31) + 1);
+    const int h0 = __builtin_amdgcn_readlane(pid_hi, 2 * (i & 31));
+    const int h1 = __builtin_amdgcn_readlane(pid_hi, 2 * (i & 31) + 1);
+    const int p0 = (i < 32) ? l0 : h0;
+    const int p1 = (i < 32) ? l1 : h1;
+    kbase = a.kp + size_t(n >= 8 ? p1 : p0) * page_stride + k_lane;
+    vbase = a.vp + size_t(q >= 2 ? p1 : p0) * page_stride + v_lane;
   };
   // Full block: every key < kend.
-  auto gload = [&](Blk& B, int kb) {
+  auto gload = [&](Blk& B, int i) {
+    const uint16_t *kbase, *vbase;
+    bases(i, kbase, vbase);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const uint16_t* src = k_src(kb + krow + 4 * t);
+      const uint16_t* src = kbase + ((krow + 4 * t) & 15) * 8;
 #pragma unroll
       for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
     }
-    const uint16_t* src = v_src(kb + 8 * q);
 #pragma unroll
-    for (int t = 0; t < 8; ++t) B.v[t] = ldg16_nt(src + 16 * t * kPage);
+    for (int t = 0; t < 8; ++t) B.v[t] = ldg16_nt(vbase + 16 * t * kPage);
   };
   // Ragged last block: keys >= kend load nothing and stay zero.
-  auto gload_tail = [&](Blk& B, int kb) {
+  auto gload_tail = [&](Blk& B, int i, int kb) {
+    const uint16_t *kbase, *vbase;
+    bases(i, kbase, vbase);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int key = kb + krow + 4 * t;
 #pragma unroll
       for (int j = 0; j < 4; ++j) B.k[t][j] = u32x4{0, 0, 0, 0};
       if (key < kend) {
-        const uint16_t* src = k_src(key);
+        const uint16_t* src = kbase + ((krow + 4 * t) & 15) * 8;
 #pragma unroll
         for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
       }
@@ -470,18 +501,18 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
 #pragma unroll
     for (int t = 0; t < 8; ++t) B.v[t] = u32x4{0, 0, 0, 0};
     if (key0 < kend) {
-      const uint16_t* src = v_src(key0);
       const int lim = kend - key0;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) B.v[t] = keep_first(ldg16(src + 16 * t * kPage), 0, lim);
+      for (int t = 0; t < 8; ++t) B.v[t] = keep_first(ldg16(vbase + 16 * t * kPage), 0, lim);
     }
   };
-  auto load = [&](Blk& B, int blk) {
-    const int kb = it.key_lo + blk * kDecodeBlock;
+  // wave-block i = global block w + 4i
+  auto load = [&](Blk& B, int i) {
+    const int kb = it.key_lo + (w + 4 * i) * kDecodeBlock;
     if (kb + kDecodeBlock <= kend)
-      gload(B, kb);
+      gload(B, i);
     else
-      gload_tail(B, kb);
+      gload_tail(B, i, kb);
   };
 
   f32x4 oacc[8];
@@ -532,18 +563,18 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.v[t]), as_bf16x8(pb), oacc[t], 0, 0, 0);
   };
 
-  // wave w takes blocks w, w+4, w+8, ...
+  // wave w takes blocks w, w+4, w+8, ... (wave-block i = block w + 4i)
   Blk A, B;
-  int b = w;
-  if (b < nblk) load(A, b);
-  while (b < nblk) {
-    if (b + 4 < nblk) load(B, b + 4);
-    consume(A, it.key_lo + b * kDecodeBlock);
-    b += 4;
-    if (b >= nblk) break;
-    if (b + 4 < nblk) load(A, b + 4);
-    consume(B, it.key_lo + b * kDecodeBlock);
-    b += 4;
+  int i = 0;
+  if (i < nmine) load(A, i);
+  while (i < nmine) {
+    if (i + 1 < nmine) load(B, i + 1);
+    consume(A, it.key_lo + (w + 4 * i) * kDecodeBlock);
+    ++i;
+    if (i >= nmine) break;
+    if (i + 1 < nmine) load(A, i + 1);
+    consume(B, it.key_lo + (w + 4 * i) * kDecodeBlock);
+    ++i;
   }
 
   // Merge the four waves. O^T register r of feature tile t holds feature 16t + 4q + r.

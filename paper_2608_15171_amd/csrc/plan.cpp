@@ -126,6 +126,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
     ksd = std::min<int64_t>(8192, std::max<int64_t>(512, ceil_div(decode_keys, target)));
   }
   ksd = std::max<int64_t>(kDecodeBlock, ceil_div(ksd, kDecodeBlock) * kDecodeBlock);
+  ksd = std::min<int64_t>(ksd, kDecodeMaxKeys);
 
   std::vector<Job> jobs;
   auto add_unit = [&](int32_t s, int32_t g, int32_t row0, int32_t pos0, int32_t npos, int kind) {

@@ -16,6 +16,7 @@ constexpr int kGroup = 8;          // query heads per KV head
 constexpr int kTilePos = 16;       // positions per prefill tile (x 8 heads = 128 rows)
 constexpr int kPrefillBlock = 64;  // keys per staged K/V block of a prefill tile
 constexpr int kDecodeBlock = 32;   // keys per block of a decode wave
+constexpr int kDecodeMaxKeys = 8192;  // longest key range of one decode item
 constexpr int kKindPrefill = 0;
 constexpr int kKindDecode = 1;
 
