@@ -239,3 +239,37 @@ def test_trace_steps_match_oracle(lib):
     for (i, l), out in res["checks"].items():
         data = TR.oracle_inputs(setup, banks, i, l)
         compare(out.astype(np.float64), oracle_out(data, 1.0 / math.sqrt(128.0)), label=f"trace step {i} layer {l}")
+
+
+# ------------------------------------------------------------------ one prompt, chunked vs single
+
+@pytest.mark.parametrize("chunk", [128, 256, 1024])
+def test_chunked_prompt_matches_oracle(lib, chunk):
+    """A prompt prefilled chunk by chunk (each chunk attending over the prefix cached
+    before it) gives the rows of the unchunked prompt; every row against the oracle."""
+    from paper_2608_15171_amd import chunk_replay as CR
+    rp = CR.Replay(1024, seed=5)
+    print(f"prompt 1024 in chunks of {chunk}", flush=True)
+    rp.run(chunk)
+    q, desc, ks, vs = rp.oracle_inputs()
+    ref = OA.mixed_step_attention(q, desc, ks, vs, rp.shape.scale, 2)
+    compare(rp.out_f64(), ref, label=f"prompt 1024 / chunk {chunk}")
+
+
+def test_chunk_replay_full_size_sampled(lib):
+    """The 16,384-token prompt as eight 2,048-token chunks and as one chunk: sampled rows
+    (chunk edges included) of both schedules against the oracle."""
+    from paper_2608_15171_amd import chunk_replay as CR
+    rp = CR.Replay(16384, seed=0)
+    g = I.rng(0, 78)
+    rows = {0, 1, 2047, 2048, 2049, 4095, 8191, 8192, 14335, 14336, 16383}
+    rows |= set(int(x) for x in g.integers(0, 16384, size=40))
+    rows = sorted(rows)
+    q, desc, ks, vs = rp.oracle_inputs()
+    ref = OA.mixed_step_attention(q, desc, ks, vs, rp.shape.scale, 2, rows=rows)
+    for chunk in (2048, 16384):
+        print(f"prompt 16384 / chunk {chunk}", flush=True)
+        rp.run(chunk)
+        out = rp.out_f64()
+        assert np.isfinite(out).all()
+        compare(out, ref, rows=rows, label=f"prompt 16384 / chunk {chunk} sampled {len(rows)} rows")

@@ -1,6 +1,7 @@
 """The seeded input generator (CPU only): bf16 rounding, determinism, descriptor packing,
 block-table structure and the four single-step workloads."""
 import numpy as np
+import pytest
 import torch
 
 from paper_2608_15171_amd import inputs as I
@@ -44,3 +45,18 @@ def test_workload_shapes():
         assert 20000 <= L <= 30000 and q.cached_len + 1024 <= L
     assert M.visible_pairs(s3) == 16384 * 8616 + 16384 * 16385 // 2
     assert abs(M.flops(s3) - 2.2560e12) / 2.256e12 < 1e-4
+
+
+def test_chunk_schedule_covers_the_prompt_once():
+    from paper_2608_15171_amd import chunk_replay as CR
+    from paper_2608_15171_amd import metrics as M
+    specs = CR.chunk_specs(16384, 2048)
+    assert len(specs) == 8
+    assert [(s.seqs[0].n_query, s.seqs[0].cached_len) for s in specs] == [(2048, 2048 * k) for k in range(8)]
+    # chunking changes the schedule, not the work: visible pairs add up to the single chunk's
+    single = CR.chunk_specs(16384, 16384)
+    assert sum(M.visible_pairs(s) for s in specs) == M.visible_pairs(single[0]) == 16384 * 16385 // 2
+    with pytest.raises(ValueError):
+        CR.chunk_specs(1000, 300)
+    bt = CR.prompt_block_table(0, 16384)
+    assert bt.shape == (1, 1024) and sorted(bt[0].tolist()) == list(range(1024))
