@@ -273,3 +273,20 @@ def test_chunk_replay_full_size_sampled(lib):
         out = rp.out_f64()
         assert np.isfinite(out).all()
         compare(out, ref, rows=rows, label=f"prompt 16384 / chunk {chunk} sampled {len(rows)} rows")
+
+
+@pytest.mark.parametrize("decode_split", [0, 1 << 20])
+def test_long_contexts_sampled(lib, decode_split):
+    """Contexts well beyond the workloads' 30k tokens: a 1,024-token chunk after 120,000
+    cached tokens and decode rows at 65,536 and 131,071 cached tokens (decode ranges at the
+    8,192-key cap, also when a larger split is asked for); sampled rows against the oracle."""
+    ppas, step, torch = lib
+    seqs = [I.Seq(1, 131071, 0), I.Seq(1, 65536, 1), I.Seq(1024, 120000, 2), I.Seq(1, 5, 3)]
+    spec = I.StepSpec("long-context", seqs)
+    print(f"long contexts, decode split {decode_split}", flush=True)
+    data, ds = run_step(lib, spec, 9, splits=(0, decode_split), spare=0)
+    rows = sample_rows(spec, I.rng(9, 77))
+    ref = oracle_out(data, ds.shape.scale, rows=rows)
+    out = ds.out_f64()
+    assert np.isfinite(out).all()
+    compare(out, ref, rows=rows, label=f"long contexts sampled {len(rows)} rows")
