@@ -114,16 +114,25 @@ def cpu_baseline(data, scale, budget_s: float):
     while True:
         rows = sample(frac)
         t0 = time.perf_counter()
-        OA.step_attention_from_data(data, scale, rows=rows)
+        ref = OA.step_attention_from_data(data, scale, rows=rows)
         dt = time.perf_counter() - t0
         if dt >= budget_s / 4 or frac >= 1.0:
             break
         frac = min(1.0, frac * max(2.0, budget_s / 2 / max(dt, 1e-3)))
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     f = flop(rows)
-    return {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(rows)} of {spec.n_rows} query rows (every decode row and the last "
-                      f"{frac:.2%} of each prefill chunk), all 16 heads, fp64 NumPy; {f:.3e} FLOP in {dt:.1f} s"}
+    rec = {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{len(rows)} of {spec.n_rows} query rows (every decode row and the last "
+                     f"{frac:.2%} of each prefill chunk), all 16 heads, fp64 NumPy; {f:.3e} FLOP in {dt:.1f} s"}
+    return rec, rows, ref
+
+
+def parity_summary(out, ref, rows):
+    """Max and mean |GPU - oracle| over the oracle's sample rows of the timed step."""
+    import numpy as np
+    err = np.abs(out[rows] - ref[rows])
+    return {"rows": len(rows), "max_abs": float(err.max()), "mean_abs": float(err.mean()),
+            "gate": {"max_abs": 1e-2, "mean_abs": 1e-3}}
 
 
 def run_trace_workload(args):
@@ -174,8 +183,8 @@ def run_trace_workload(args):
     if not args.no_cpu_baseline:
         data = TR.oracle_inputs(setup, banks, big, 0)
         cb = cpu_baseline(data, 1.0 / math.sqrt(128.0), args.cpu_seconds)
-        cb["sample"] = "largest step of the trace, layer 0: " + cb["sample"]
-        rec["cpu_baseline"] = cb
+        cb[0]["sample"] = "largest step of the trace, layer 0: " + cb[0]["sample"]
+        rec["cpu_baseline"] = cb[0]
     print(json.dumps(rec), flush=True)
 
 
@@ -237,7 +246,8 @@ def run_chunks_workload(args):
         spec = I.StepSpec(f"prompt{P}", [I.Seq(P, 0, 0)])
         empty = np.zeros((0, I.HKV, I.HEAD_DIM), dtype=np.uint16)
         data = I.StepData(spec, desc, q, ks[0], vs[0], [empty], [empty])
-        rec["cpu_baseline"] = cpu_baseline(data, rp.shape.scale, args.cpu_seconds)
+        rec["cpu_baseline"], rows, ref = cpu_baseline(data, rp.shape.scale, args.cpu_seconds)
+        rec["parity"] = parity_summary(rp.out_f64(), ref, rows)
     print(json.dumps(rec), flush=True)
 
 
@@ -369,7 +379,8 @@ def main():
         },
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(data, ds.shape.scale, args.cpu_seconds)
+        rec["cpu_baseline"], rows, ref = cpu_baseline(data, ds.shape.scale, args.cpu_seconds)
+        rec["parity"] = parity_summary(ds.out_f64(), ref, rows)
     print(json.dumps(rec), flush=True)
 
 
