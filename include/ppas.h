@@ -164,6 +164,18 @@ int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n
 ppas_status ppas_set_split_keys(int32_t prefill_split, int32_t decode_split);
 
 /*
+ * Planner tuning (process-wide). The packed launch comes in two shapes: prefill
+ * tiles of 16 positions on four-wave workgroups, or of 32 positions on
+ * eight-wave workgroups (each staged K/V block then serves twice the rows). By
+ * default (0) each step picks 32 only when its 32-position tiles reach two per
+ * compute unit and decode rows are a small share of its work; 16 or 32 forces
+ * the shape. Affects plans made after the call, including
+ * ppas_attn_workspace_bytes and ppas_plan_items (whose npos then reaches 32).
+ * Returns PPAS_EINVAL for any other value.
+ */
+ppas_status ppas_set_tile_positions(int32_t tile_positions);
+
+/*
  * Profiling hook (process-wide). When both are non-NULL, the next
  * ppas_attn_step calls record `start_event` on their stream immediately before
  * the packed attention kernel is launched and `stop_event` immediately after it

@@ -15,7 +15,7 @@ namespace ppas {
 hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp, const uint16_t* vp,
                             const int32_t* bt, int32_t bt_stride, int32_t hq, int32_t hkv, float scale,
                             const WorkItem* items, int n_items, const CombineItem* comb, int n_comb,
-                            float2* part_ml, float* part_acc, hipStream_t stream,
+                            float2* part_ml, float* part_acc, int tile_pos, hipStream_t stream,
                             hipEvent_t ev_start, hipEvent_t ev_stop);
 hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
                             const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
@@ -137,6 +137,12 @@ ppas_status ppas_set_split_keys(int32_t prefill_split, int32_t decode_split) {
   return PPAS_OK;
 }
 
+ppas_status ppas_set_tile_positions(int32_t tile_positions) {
+  if (tile_positions != 0 && tile_positions != kTilePosSmall && tile_positions != kTilePosLarge) return PPAS_EINVAL;
+  set_tile_positions(tile_positions);
+  return PPAS_OK;
+}
+
 int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs, int32_t num_cus,
                         int32_t* items_out, int32_t capacity) {
   try {
@@ -224,7 +230,7 @@ ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q, co
         static_cast<const uint16_t*>(v_pages), block_table_dev, bt_stride, shape->n_q_heads, shape->n_kv_heads,
         shape->scale, reinterpret_cast<const WorkItem*>(ws + plan.off_items), int(plan.items.size()),
         reinterpret_cast<const CombineItem*>(ws + plan.off_combine), int(plan.combine.size()),
-        reinterpret_cast<float2*>(ws + plan.off_ml), reinterpret_cast<float*>(ws + plan.off_acc), stream,
+        reinterpret_cast<float2*>(ws + plan.off_ml), reinterpret_cast<float*>(ws + plan.off_acc), plan.tile_pos, stream,
         static_cast<hipEvent_t>(g_ev_start.load()), static_cast<hipEvent_t>(g_ev_stop.load()));
     return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
   } catch (...) {

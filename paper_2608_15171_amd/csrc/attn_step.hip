@@ -46,7 +46,12 @@ struct StepArgs {
   float scale_log2;     // softmax scale * log2(e)
 };
 
-constexpr int kThreads = 256;
+// The kernel comes in two shapes, by waves per workgroup W: W = 4 (prefill tiles
+// of 16 positions, two workgroups per CU) and W = 8 (tiles of 32 positions, one
+// workgroup per CU; each staged K/V byte then serves 256 rows). The planner
+// picks one per step.
+template <int kW>
+constexpr int threads_of() { return 64 * kW; }
 constexpr int kRegion = 1024;              // one wave's 64 x 16-byte LDS transfer
 constexpr int kBlockBytes = 16 * kRegion;  // K (or V) of one 64-key block
 constexpr float kNegInf = -__builtin_inff();
@@ -115,9 +120,9 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
 }
 
 // ---------------------------------------------------------------------------
-// Prefill tile: 16 positions x 8 query heads = 128 rows; wave w owns positions
+// Prefill tile: 4W positions x 8 query heads = 32W rows; wave w owns positions
 // 4w..4w+3 (32 rows, one per lane column n = lane & 31; lanes n and n+32 share
-// a row). S^T = K Q^T and O^T += V^T P^T on 32x32x16 MFMAs, so every softmax
+// a row). All W waves read the same staged K/V blocks. S^T = K Q^T and O^T += V^T P^T on 32x32x16 MFMAs, so every softmax
 // reduction stays inside a lane plus one exchange across the two half-waves.
 //
 // MFMA row m of a 32-key tile reads key pi(m), which swaps the middle two groups
@@ -125,7 +130,8 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
 // the P^T operand of k-step s.
 //
 // LDS holds each 64-key block in MFMA operand order, written straight from
-// global memory by 16-byte LDS transfers: K region (t, j) = 8t + j holds, at
+// global memory by 16-byte LDS transfers (16 regions of K and 16 of V per block,
+// 16/W of each per wave): K region (t, j) = 8t + j holds, at
 // 16 L, lane L's A chunk for key tile t and k-step j (key 32t + pi(L & 31),
 // features 16j + 8(L >> 5) .. +7); V region (tt, s) = 4tt + s holds lane L's V^T
 // chunk (feature 32tt + (L & 31), keys 16s + 8(L >> 5) .. +7). Every operand
@@ -159,24 +165,37 @@ __device__ __forceinline__ PageIds page_ids(const PrefillCtx& c, int blk) {
   return r;
 }
 
-// This wave's four K transfers of a block: regions 4w..4w+3, i.e. key tile w/2
-// (pages 2(w/2) and 2(w/2)+1 of the block) and k-steps 4(w&1)..4(w&1)+3.
+// This wave's K transfers of a block: regions R w .. R w + R-1 (R = 16/W), all in
+// key tile t = R w / 8 (pages 2t and 2t+1 of the block), k-steps (R w mod 8) + i.
+template <int kW>
 __device__ __forceinline__ void dma_k(const PrefillCtx& c, const PageIds& pg, char* kbuf) {
-  const int lo = (c.w >> 1) ? pg.p[2] : pg.p[0];
-  const int hi = (c.w >> 1) ? pg.p[3] : pg.p[1];
+  constexpr int R = 16 / kW;
+  const bool t1 = (R * c.w) >> 3;
+  const int lo = t1 ? pg.p[2] : pg.p[0];
+  const int hi = t1 ? pg.p[3] : pg.p[1];
   const uint16_t* lo_base = c.a->kp + size_t(lo) * c.page_stride;
   const uint16_t* hi_base = c.a->kp + size_t(hi) * c.page_stride;
   const uint16_t* base = ((c.pi_n >> 4) ? hi_base : lo_base) + c.k_lane_off;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dma16(base + 2 * i * kChunkElems, kbuf + (4 * c.w + i) * kRegion);
+  for (int i = 0; i < R; ++i) dma16(base + 2 * i * kChunkElems, kbuf + (R * c.w + i) * kRegion);
 }
 
-// This wave's four V transfers of a block: regions 4w..4w+3, i.e. feature tile w
-// over the block's four pages.
+// This wave's V transfers of a block: regions R w .. R w + R-1, all in feature
+// tile tt = R w / 4, over pages s = (R w mod 4) + i of the block.
+template <int kW>
 __device__ __forceinline__ void dma_v(const PrefillCtx& c, const PageIds& pg, char* vbuf) {
+  constexpr int R = 16 / kW;
+  if constexpr (R == 4) {
 #pragma unroll
-  for (int s = 0; s < 4; ++s)
-    dma16(c.a->vp + size_t(pg.p[s]) * c.page_stride + c.v_lane_off, vbuf + (4 * c.w + s) * kRegion);
+    for (int s = 0; s < 4; ++s)
+      dma16(c.a->vp + size_t(pg.p[s]) * c.page_stride + c.v_lane_off, vbuf + (4 * c.w + s) * kRegion);
+  } else {
+    static_assert(R == 2, "four or eight waves");
+    const int p0 = (c.w & 1) ? pg.p[2] : pg.p[0];
+    const int p1 = (c.w & 1) ? pg.p[3] : pg.p[1];
+    dma16(c.a->vp + size_t(p0) * c.page_stride + c.v_lane_off, vbuf + (2 * c.w) * kRegion);
+    dma16(c.a->vp + size_t(p1) * c.page_stride + c.v_lane_off, vbuf + (2 * c.w + 1) * kRegion);
+  }
 }
 
 __device__ __forceinline__ void qk_block(const char* kbuf, int lane, const bf16x8 (&qf)[8], f32x16 (&S)[2]) {
@@ -235,7 +254,9 @@ __device__ __forceinline__ void pv_block(const char* vbuf, int lane, int h, cons
     }
 }
 
+template <int kW>
 __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& it, char* smem) {
+  constexpr int R = 16 / kW;   // transfers of K (and of V) per wave per block
   const int tid = threadIdx.x;
   PrefillCtx c;
   c.a = &a;
@@ -252,10 +273,10 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
   c.page_stride = size_t(a.hkv) * kPageElems;
   {
     const uint32_t head_off = uint32_t(it.kvh) * kPageElems;
-    // K: chunk 2j + h of k-step j = 4(w&1) + i, slot pi(n) & 15
-    c.k_lane_off = head_off + (8 * (c.w & 1) + c.h) * kChunkElems + (c.pi_n & 15) * 8;
-    // V: feature 32w + n, slots 8h..8h+7
-    c.v_lane_off = head_off + (32 * c.w + c.n) * kPage + 8 * c.h;
+    // K: chunk 2j + h of k-step j = (R w mod 8) + i, slot pi(n) & 15
+    c.k_lane_off = head_off + (2 * ((R * c.w) & 7) + c.h) * kChunkElems + (c.pi_n & 15) * 8;
+    // V: feature 32 tt + n with tt = R w / 4, slots 8h..8h+7
+    c.v_lane_off = head_off + (32 * ((R * c.w) >> 2) + c.n) * kPage + 8 * c.h;
   }
   c.key_lo = it.key_lo;
   c.kend = it.key_hi;
@@ -294,9 +315,9 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
   // prologue: K(0), K(1), V(0) in flight; page ids of blocks 1 and 2 kept for the loop
   const PageIds pg0 = page_ids(c, 0);
   PageIds pg1 = page_ids(c, 1), pg2 = page_ids(c, 2);
-  dma_k(c, pg0, kbuf(0));
-  dma_k(c, pg1, kbuf(1));
-  dma_v(c, pg0, vbuf(0));
+  dma_k<kW>(c, pg0, kbuf(0));
+  dma_k<kW>(c, pg1, kbuf(1));
+  dma_v<kW>(c, pg0, vbuf(0));
   wait_vmem();
   __syncthreads();
 
@@ -306,8 +327,8 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 
   // Main loop: blocks b and b + 1 both unmasked.
   auto main_iter = [&](int b, f32x16 (&Scur)[2], f32x16 (&Snext)[2]) {
-    dma_k(c, pg2, kbuf(b));
-    dma_v(c, pg1, vbuf(b + 1));
+    dma_k<kW>(c, pg2, kbuf(b));
+    dma_v<kW>(c, pg1, vbuf(b + 1));
     pg1 = pg2;
     pg2 = page_ids(c, b + 3);
     const float m_use = (m_run == kNegInf) ? 0.f : m_run;
@@ -347,8 +368,8 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
         }
       rescale_if_grown(block_max(SA) * sl2, m_run, l_run, O);
     }
-    if (b + 2 < nblk) dma_k(c, pg2, kbuf(b));
-    if (b + 1 < nblk) dma_v(c, pg1, vbuf(b + 1));
+    if (b + 2 < nblk) dma_k<kW>(c, pg2, kbuf(b));
+    if (b + 1 < nblk) dma_v<kW>(c, pg1, vbuf(b + 1));
     pg1 = pg2;
     pg2 = page_ids(c, b + 3);
     const float m_use = (m_run == kNegInf) ? 0.f : m_run;
@@ -397,7 +418,7 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 
 // ---------------------------------------------------------------------------
 // Decode item: one query row (8 heads) of one KV head over keys [key_lo, key_hi).
-// The four waves take interleaved 32-key blocks and stream K/V from HBM straight
+// The W waves take interleaved 32-key blocks and stream K/V from HBM straight
 // into 16x16x32 MFMA operands (heads in the N dimension, padded 8 -> 16), then
 // merge their running (m, l, acc) through LDS.
 // Lane (n = lane & 15, q = lane >> 4): K rows of tile t are keys 8*(m/4) + 4t + m%4,
@@ -407,7 +428,10 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 // order 32q + 8j + i (k-step j) for both the Q and K operands, so lane q's K
 // operand is chunks 4q..4q+3 of its key.
 // ---------------------------------------------------------------------------
+template <int kW>
 __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it, char* smem) {
+  constexpr int kWaves = kW;
+  constexpr int kThreads = threads_of<kW>();
   const int tid = threadIdx.x;
   // the wave index is uniform; saying so keeps per-wave control flow scalar
   const int lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -426,23 +450,23 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   const size_t page_stride = size_t(a.hkv) * kPageElems;
   const int kend = it.key_hi;
   const int nblk = (kend - it.key_lo + kDecodeBlock - 1) / kDecodeBlock;
-  const int nmine = nblk > w ? (nblk - w + 3) / 4 : 0;   // blocks w, w+4, ... of this wave
+  const int nmine = nblk > w ? (nblk - w + kWaves - 1) / kWaves : 0;   // blocks w, w+W, ... of this wave
 
   const int krow = 8 * (n >> 2) + (n & 3);   // + 4t for tile t: key row of the K operand
 
   // Page ids. Item key ranges start on 32-key boundaries, so block b covers
-  // pages first + 2b and first + 2b + 1. This wave's i-th block is b = w + 4i;
-  // lane L of a page-id register holds page 2(w + 4(i0 + L/2)) + (L & 1) for the
+  // pages first + 2b and first + 2b + 1. This wave's i-th block is b = w + Wi;
+  // lane L of a page-id register holds page 2(w + W(i0 + L/2)) + (L & 1) for the
   // register's base block i0, so one register serves 32 blocks and the ids of a
   // block come out with two lane reads, with no load on the loop's critical path.
   const int first_page = it.key_lo >> 4;
   const int last_page = (kend - 1) >> 4;
   auto load_pids = [&](int i0) {
-    const int blk = w + 4 * (i0 + (lane >> 1));
+    const int blk = w + kWaves * (i0 + (lane >> 1));
     return btrow[min(first_page + 2 * blk + (lane & 1), last_page)];
   };
   // The planner caps decode key ranges at kDecodeMaxKeys, so a wave has at most 64 blocks.
-  static_assert(kDecodeMaxKeys <= 4 * 64 * kDecodeBlock, "two page-id registers per wave");
+  static_assert(kDecodeMaxKeys <= kWaves * 64 * kDecodeBlock, "two page-id registers per wave");
   const int pid_lo = load_pids(0), pid_hi = load_pids(32);
   // Complete the page-id loads here, once (the Q loads stay in flight), so the
   // loop never waits on them.
@@ -506,9 +530,9 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       for (int t = 0; t < 8; ++t) B.v[t] = keep_first(ldg16(vbase + 16 * t * kPage), 0, lim);
     }
   };
-  // wave-block i = global block w + 4i
+  // wave-block i = global block w + W i
   auto load = [&](Blk& B, int i) {
-    const int kb = it.key_lo + (w + 4 * i) * kDecodeBlock;
+    const int kb = it.key_lo + (w + kWaves * i) * kDecodeBlock;
     if (kb + kDecodeBlock <= kend)
       gload(B, i);
     else
@@ -563,26 +587,26 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.v[t]), as_bf16x8(pb), oacc[t], 0, 0, 0);
   };
 
-  // wave w takes blocks w, w+4, w+8, ... (wave-block i = block w + 4i)
+  // wave w takes blocks w, w+W, w+2W, ... (wave-block i = block w + W i)
   Blk A, B;
   int i = 0;
   if (i < nmine) load(A, i);
   while (i < nmine) {
     if (i + 1 < nmine) load(B, i + 1);
-    consume(A, it.key_lo + (w + 4 * i) * kDecodeBlock);
+    consume(A, it.key_lo + (w + kWaves * i) * kDecodeBlock);
     ++i;
     if (i >= nmine) break;
     if (i + 1 < nmine) load(A, i + 1);
-    consume(B, it.key_lo + (w + 4 * i) * kDecodeBlock);
+    consume(B, it.key_lo + (w + kWaves * i) * kDecodeBlock);
     ++i;
   }
 
-  // Merge the four waves. O^T register r of feature tile t holds feature 16t + 4q + r.
+  // Merge the waves. O^T register r of feature tile t holds feature 16t + 4q + r.
   float l_w = l_run + __shfl_xor(l_run, 16);
   l_w += __shfl_xor(l_w, 32);
-  float* wo = reinterpret_cast<float*>(smem);                 // [4][8][128]
-  float* wm = wo + 4 * kGroup * kHeadDim;                      // [4][8]
-  float* wl = wm + 4 * kGroup;                                 // [4][8]
+  float* wo = reinterpret_cast<float*>(smem);                 // [W][8][128]
+  float* wm = wo + kWaves * kGroup * kHeadDim;                 // [W][8]
+  float* wl = wm + kWaves * kGroup;                            // [W][8]
   if (hvalid) {
 #pragma unroll
     for (int t = 0; t < 8; ++t)
@@ -593,41 +617,48 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     }
   }
   __syncthreads();
-  const int head = tid >> 5;            // 0..7
-  const int d0 = (tid & 31) * 4;
+  // thread t finishes head t / (kThreads/8), kF consecutive features
+  constexpr int kTPH = kThreads / kGroup;   // threads per head
+  constexpr int kF = kHeadDim / kTPH;       // features per thread: 4 or 2
+  const int head = tid / kTPH;
+  const int d0 = (tid % kTPH) * kF;
   float M = kNegInf;
 #pragma unroll
-  for (int v = 0; v < 4; ++v) M = fmaxf(M, wm[v * kGroup + head]);
+  for (int v = 0; v < kWaves; ++v) M = fmaxf(M, wm[v * kGroup + head]);
   const float M_use = (M == kNegInf) ? 0.f : M;
   float L = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[kF] = {};
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
+  for (int v = 0; v < kWaves; ++v) {
     const float f = fast_exp2(wm[v * kGroup + head] - M_use);
     L += f * wl[v * kGroup + head];
-    acc += f * *reinterpret_cast<const f32x4*>(wo + (v * kGroup + head) * kHeadDim + d0);
+    const float* src = wo + (v * kGroup + head) * kHeadDim + d0;
+#pragma unroll
+    for (int e = 0; e < kF; ++e) acc[e] += f * src[e];
   }
   if (it.part < 0) {
     const float inv = 1.f / L;
     uint16_t* orow = a.out + (size_t(it.row0) * a.hq + it.kvh * kGroup + head) * kHeadDim + d0;
-    u32x2 v;
-    v[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-    v[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-    *reinterpret_cast<u32x2*>(orow) = v;
+#pragma unroll
+    for (int e = 0; e < kF; e += 2)
+      *reinterpret_cast<uint32_t*>(orow + e) = pack_bf16x2(acc[e] * inv, acc[e + 1] * inv);
   } else {
     const int slot = it.part + head;
-    *reinterpret_cast<f32x4*>(a.part_acc + size_t(slot) * kHeadDim + d0) = acc;
-    if ((tid & 31) == 0) a.part_ml[slot] = make_float2(M, L);
+    float* dst = a.part_acc + size_t(slot) * kHeadDim + d0;
+#pragma unroll
+    for (int e = 0; e < kF; ++e) dst[e] = acc[e];
+    if ((tid % kTPH) == 0) a.part_ml[slot] = make_float2(M, L);
   }
 }
 
-__global__ __launch_bounds__(kThreads, 2) void attn_step_kernel(StepArgs a) {
+template <int kW>
+__global__ __launch_bounds__(threads_of<kW>(), kW == 4 ? 2 : 1) void attn_step_kernel(StepArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[4 * kBlockBytes];
   const WorkItem it = a.items[blockIdx.x];
   if ((it.npos_kind >> 16) == kKindDecode)
-    decode_row(a, it, smem);
+    decode_row<kW>(a, it, smem);
   else
-    prefill_tile(a, it, smem);
+    prefill_tile<kW>(a, it, smem);
 }
 
 // Merge split partials: for local row r of a combine item with partials
@@ -635,7 +666,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_step_kernel(StepArgs a) {
 // Block (item, y) handles rows 8y..8y+7 of the item; 32 lanes per row, 4
 // features per lane.
 constexpr int kCombineRowsPerBlock = 8;
-__global__ __launch_bounds__(kThreads) void combine_kernel(const CombineItem* items, const float2* part_ml,
+constexpr int kCombineThreads = 32 * kCombineRowsPerBlock;
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineItem* items, const float2* part_ml,
                                                            const float* part_acc, uint16_t* out, int hq) {
   const CombineItem ci = items[blockIdx.x];
   const int rows = ci.npos * kGroup;
@@ -666,8 +698,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(const CombineItem* it
 hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp, const uint16_t* vp,
                             const int32_t* bt, int32_t bt_stride, int32_t hq, int32_t hkv, float scale,
                             const WorkItem* items, int n_items, const CombineItem* comb, int n_comb,
-                            float2* part_ml, float* part_acc, hipStream_t stream,
+                            float2* part_ml, float* part_acc, int tile_pos, hipStream_t stream,
                             hipEvent_t ev_start, hipEvent_t ev_stop) {
+  if (tile_pos != kTilePosSmall && tile_pos != kTilePosLarge) return hipErrorInvalidValue;
   if (n_items > 0) {
     StepArgs a;
     a.q = q;
@@ -683,14 +716,18 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
     a.hkv = hkv;
     a.scale_log2 = scale * 1.4426950408889634f;
     if (ev_start && hipEventRecord(ev_start, stream) != hipSuccess) return hipGetLastError();
-    hipLaunchKernelGGL(attn_step_kernel, dim3(n_items), dim3(kThreads), 0, stream, a);
+    if (tile_pos == kTilePosLarge)
+      hipLaunchKernelGGL(attn_step_kernel<8>, dim3(n_items), dim3(threads_of<8>()), 0, stream, a);
+    else
+      hipLaunchKernelGGL(attn_step_kernel<4>, dim3(n_items), dim3(threads_of<4>()), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess) return hipGetLastError();
   }
   if (n_comb > 0) {
-    const int ymax = kTilePos * kGroup / kCombineRowsPerBlock;
-    hipLaunchKernelGGL(combine_kernel, dim3(n_comb, ymax), dim3(kThreads), 0, stream, comb, part_ml, part_acc, out, hq);
+    const int ymax = tile_pos * kGroup / kCombineRowsPerBlock;
+    hipLaunchKernelGGL(combine_kernel, dim3(n_comb, ymax), dim3(kCombineThreads), 0, stream, comb, part_ml, part_acc,
+                       out, hq);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -11,6 +11,7 @@ namespace ppas {
 namespace {
 std::atomic<int32_t> g_prefill_split{0};
 std::atomic<int32_t> g_decode_split{0};
+std::atomic<int32_t> g_tile_pos{0};
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -19,6 +20,12 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 #define PPAS_INTERLEAVE_RATIO 0.5
 #endif
 constexpr double kInterleaveRatio = PPAS_INTERLEAVE_RATIO;
+// largest decode cost, relative to the prefill cost, at which a step may use
+// 32-position prefill tiles
+#ifndef PPAS_LARGE_TILE_DECODE_SHARE
+#define PPAS_LARGE_TILE_DECODE_SHARE 0.05
+#endif
+constexpr double kLargeTileDecodeShare = PPAS_LARGE_TILE_DECODE_SHARE;
 // when interleaving, prefill advances at this multiple of the decode fraction
 #ifndef PPAS_INTERLEAVE_BIAS
 #define PPAS_INTERLEAVE_BIAS 1.0
@@ -29,6 +36,8 @@ constexpr double kInterleaveRatio = PPAS_INTERLEAVE_RATIO;
 #endif
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 }  // namespace
+
+void set_tile_positions(int32_t tile_pos) { g_tile_pos.store(tile_pos); }
 
 void set_split_keys(int32_t prefill, int32_t decode) {
   g_prefill_split.store(prefill);
@@ -101,18 +110,40 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   if (num_cus <= 0) num_cus = 256;
 
   // Total work, to size the key splits so that the launch has several
-  // workgroups per compute unit.
-  int64_t prefill_keys = 0, decode_keys = 0;
+  // workgroups per compute unit: keys summed over prefill tiles (of either
+  // size) and over decode rows.
+  auto prefill_keys_for = [&](int32_t tile) {
+    int64_t keys = 0;
+    for (int32_t s = 0; s < n_seqs; ++s) {
+      const ppas_seq& q = seqs[s];
+      if (q.n_query == 1) continue;
+      for (int32_t t0 = 0; t0 < q.n_query; t0 += tile) keys += int64_t(q.cached_len) + std::min(q.n_query, t0 + tile);
+    }
+    return keys * hkv;
+  };
+  int64_t decode_keys = 0, large_tiles = 0;
   for (int32_t s = 0; s < n_seqs; ++s) {
     const ppas_seq& q = seqs[s];
-    if (q.n_query == 1) {
+    if (q.n_query == 1)
       decode_keys += int64_t(q.cached_len + 1) * hkv;
-    } else {
-      for (int32_t t0 = 0; t0 < q.n_query; t0 += kTilePos)
-        prefill_keys += int64_t(q.cached_len) + std::min(q.n_query, t0 + kTilePos);
-    }
+    else
+      large_tiles += ceil_div(q.n_query, kTilePosLarge) * hkv;
   }
-  prefill_keys *= hkv;
+
+  // Tile shape. The eight-wave kernel stages each K/V block once for 256 rows
+  // instead of 128, which pays when the step's prefill alone fills the chip with
+  // 32-position tiles (two per CU before any key split) and decode rows are a
+  // small share of the work (a workgroup then holds a whole CU, so a prefill
+  // tile no longer shares its CU with a decode item).
+  int32_t tile = g_tile_pos.load();
+  if (tile != kTilePosSmall && tile != kTilePosLarge) {
+    const int64_t small_keys = prefill_keys_for(kTilePosSmall);
+    const bool big = large_tiles >= int64_t(2) * num_cus;
+    const bool few_decodes = double(decode_keys) * 2.0 < kLargeTileDecodeShare * double(small_keys);
+    tile = (big && few_decodes) ? kTilePosLarge : kTilePosSmall;
+  }
+  plan.tile_pos = tile;
+  const int64_t prefill_keys = prefill_keys_for(tile);
 
   int64_t ksp = g_prefill_split.load();
   if (ksp <= 0) {
@@ -162,8 +193,8 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
       if (q.n_query == 1) {
         add_unit(s, g, q.query_start, q.cached_len, 1, kKindDecode);
       } else {
-        for (int32_t t0 = 0; t0 < q.n_query; t0 += kTilePos)
-          add_unit(s, g, q.query_start + t0, q.cached_len + t0, std::min(kTilePos, q.n_query - t0), kKindPrefill);
+        for (int32_t t0 = 0; t0 < q.n_query; t0 += tile)
+          add_unit(s, g, q.query_start + t0, q.cached_len + t0, std::min(tile, q.n_query - t0), kKindPrefill);
       }
     }
   }

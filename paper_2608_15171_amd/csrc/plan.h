@@ -13,7 +13,10 @@ namespace ppas {
 constexpr int kHeadDim = 128;
 constexpr int kPage = 16;
 constexpr int kGroup = 8;          // query heads per KV head
-constexpr int kTilePos = 16;       // positions per prefill tile (x 8 heads = 128 rows)
+// positions per prefill tile (x 8 heads): 16 for the four-wave kernel, 32 for
+// the eight-wave one; each plan uses one of them
+constexpr int kTilePosSmall = 16;
+constexpr int kTilePosLarge = 32;
 constexpr int kPrefillBlock = 64;  // keys per staged K/V block of a prefill tile
 constexpr int kDecodeBlock = 32;   // keys per block of a decode wave
 constexpr int kDecodeMaxKeys = 8192;  // longest key range of one decode item
@@ -39,6 +42,7 @@ struct CombineItem {
 static_assert(sizeof(CombineItem) == 32, "CombineItem is 32 bytes");
 
 struct Plan {
+  int tile_pos = kTilePosSmall;    // prefill tile positions, selects the kernel shape
   std::vector<WorkItem> items;     // in launch order
   std::vector<CombineItem> combine;
   int64_t part_slots = 0;
@@ -53,5 +57,8 @@ ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_se
 void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, Plan& plan);
 
 void set_split_keys(int32_t prefill, int32_t decode);
+
+// 0: choose the tile size per step; 16 or 32: force it.
+void set_tile_positions(int32_t tile_pos);
 
 }  // namespace ppas

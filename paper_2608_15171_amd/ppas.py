@@ -74,6 +74,8 @@ _lib.ppas_set_profile_events.restype = ctypes.c_int
 _lib.ppas_set_profile_events.argtypes = [_vp, _vp]
 _lib.ppas_set_split_keys.restype = ctypes.c_int
 _lib.ppas_set_split_keys.argtypes = [_i32, _i32]
+_lib.ppas_set_tile_positions.restype = ctypes.c_int
+_lib.ppas_set_tile_positions.argtypes = [_i32]
 
 
 def status_string(status: int) -> str:
@@ -168,6 +170,11 @@ def plan_items(shape: Shape, desc, num_cus: int = 256) -> np.ndarray:
 
 def set_split_keys(prefill: int = 0, decode: int = 0) -> None:
     _check(_lib.ppas_set_split_keys(int(prefill), int(decode)), "ppas_set_split_keys")
+
+
+def set_tile_positions(tile_positions: int = 0) -> None:
+    """Force 16- or 32-position prefill tiles (the four- or eight-wave kernel); 0 = per-step choice."""
+    _check(_lib.ppas_set_tile_positions(int(tile_positions)), "ppas_set_tile_positions")
 
 
 def set_profile_events(start_event, stop_event) -> None:

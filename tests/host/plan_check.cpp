@@ -101,7 +101,8 @@ void check_plan(const Step& st, const Plan& plan) {
     const ppas_seq& q = st.seqs[size_t(it.seq)];
     CHECK(it.kvh >= 0 && it.kvh < hkv);
     CHECK(kind == (q.n_query == 1 ? kKindDecode : kKindPrefill));
-    CHECK(npos >= 1 && npos <= kTilePos);
+    CHECK(npos >= 1 && npos <= plan.tile_pos);
+    CHECK(plan.tile_pos == kTilePosSmall || plan.tile_pos == kTilePosLarge);
     CHECK(it.row0 >= q.query_start && it.row0 + npos <= q.query_start + q.n_query);
     CHECK(it.pos0 == q.cached_len + (it.row0 - q.query_start));
     CHECK(it.key_lo >= 0 && it.key_lo < it.key_hi && it.key_hi <= it.pos0 + npos);
@@ -139,7 +140,7 @@ void check_plan(const Step& st, const Plan& plan) {
   // combine items: one per split (row block, KV head), each split item accounted for
   int64_t comb_slots = 0;
   for (const CombineItem& c : plan.combine) {
-    CHECK(c.nsplit >= 2 && c.npos >= 1 && c.npos <= kTilePos);
+    CHECK(c.nsplit >= 2 && c.npos >= 1 && c.npos <= plan.tile_pos);
     CHECK(c.part >= 0 && int64_t(c.part) + int64_t(c.nsplit) * c.npos * kGroup <= plan.part_slots);
     comb_slots += int64_t(c.nsplit) * c.npos * kGroup;
   }
@@ -164,11 +165,13 @@ void fuzz() {
     CHECK(validate(&sh, st.seqs.data(), n, st.bt.data(), st.stride, true) == PPAS_OK);
     const auto& sp = splits[t % 4];
     set_split_keys(sp[0], sp[1]);
+    set_tile_positions((t / 4) % 3 == 0 ? 0 : (t / 4) % 3 == 1 ? kTilePosSmall : kTilePosLarge);
     Plan plan;
     make_plan(sh, st.seqs.data(), n, cus[t % 5], plan);
     check_plan(st, plan);
   }
   set_split_keys(0, 0);
+  set_tile_positions(0);
 }
 
 void invalid() {

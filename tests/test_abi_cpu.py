@@ -128,14 +128,34 @@ def check_coverage(spec, items):
 
 @pytest.mark.parametrize("seed", range(8))
 @pytest.mark.parametrize("splits", [(0, 0), (64, 32), (128, 96)])
-def test_plan_covers_visible_keys_once(seed, splits):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_plan_covers_visible_keys_once(seed, splits, tile):
     spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
     ppas.set_split_keys(*splits)
+    ppas.set_tile_positions(tile)
     try:
         items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
     finally:
         ppas.set_split_keys(0, 0)
+        ppas.set_tile_positions(0)
     check_coverage(spec, items)
+    assert items[items[:, 0] == 0, 5].max(initial=0) <= tile
+
+
+def test_tile_shape_choice():
+    """32-position tiles only for steps whose prefill fills the chip on its own and whose
+    decode work is a small share; every other step keeps 16-position tiles."""
+    def npos_max(spec):
+        items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
+        return int(items[items[:, 0] == 0, 5].max())
+    assert npos_max(I.config_large_budget(0)) == 32        # one 16,384-token chunk
+    assert npos_max(I.config_small_budget(0)) == 16        # 2,048-token chunk: too few large tiles
+    assert npos_max(I.config_small(0)) == 16
+    assert npos_max(I.config_high_pressure(0)) == 16       # decode-heavy
+    heavy = I.StepSpec("16k+decodes", [I.Seq(1, 25000, i) for i in range(40)] + [I.Seq(16384, 8616, 99)])
+    assert npos_max(heavy) == 16
+    with pytest.raises(ppas.PPASError):
+        ppas.set_tile_positions(24)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])

@@ -47,11 +47,13 @@ def compare(gpu, ref, rows=None, label=""):
     assert rel <= ROW_REL, f"{label}: row relative L2 {rel}"
 
 
-def run_step(lib, spec, seed, permute=True, splits=(0, 0), pool_fill=SENTINEL, spare=5):
+def run_step(lib, spec, seed, permute=True, splits=(0, 0), pool_fill=SENTINEL, spare=5, tile=0):
+    """tile: 16 or 32 forces the four- or eight-wave kernel; 0 lets the planner choose."""
     ppas, step, torch = lib
     data = I.make_step_data(spec, seed)
     bt, npages = I.make_block_table(spec, seed, permute=permute, spare_pages=spare)
     ppas.set_split_keys(*splits)
+    ppas.set_tile_positions(tile)
     try:
         ds = step.DeviceStep(data, bt, npages, pool_fill=pool_fill)
         ds.fill_history()
@@ -59,6 +61,7 @@ def run_step(lib, spec, seed, permute=True, splits=(0, 0), pool_fill=SENTINEL, s
         torch.cuda.synchronize()
     finally:
         ppas.set_split_keys(0, 0)
+        ppas.set_tile_positions(0)
     return data, ds
 
 
@@ -105,11 +108,13 @@ def test_kv_append_history_round_trip(lib):
 
 @pytest.mark.parametrize("seed", range(8))
 @pytest.mark.parametrize("splits", [(0, 0), (64, 32), (192, 96)])
-def test_attention_fuzz(lib, seed, splits):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_attention_fuzz(lib, seed, splits, tile):
     spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
-    print(f"fuzz seed={seed} splits={splits} seqs={[(s.n_query, s.cached_len) for s in spec.seqs]}", flush=True)
-    data, ds = run_step(lib, spec, seed, splits=splits)
-    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"fuzz{seed}/{splits}")
+    print(f"fuzz seed={seed} splits={splits} tile={tile} seqs={[(s.n_query, s.cached_len) for s in spec.seqs]}",
+          flush=True)
+    data, ds = run_step(lib, spec, seed, splits=splits, tile=tile)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"fuzz{seed}/{splits}/tile{tile}")
 
 
 def test_attention_small_config(lib):
@@ -131,36 +136,45 @@ def test_attention_edge_cases(lib):
             I.Seq(1, 63, 5), I.Seq(1, 64, 6), I.Seq(33, 1, 7), I.Seq(3, 127, 8)]
     spec = I.StepSpec("edges", seqs)
     for splits in [(0, 0), (64, 32)]:
-        data, ds = run_step(lib, spec, 21, splits=splits)
-        out = ds.out_f64()
-        compare(out, oracle_out(data, ds.shape.scale), label=f"edges{splits}")
+        for tile in (16, 32):
+            print(f"edges splits={splits} tile={tile}", flush=True)
+            data, ds = run_step(lib, spec, 21, splits=splits, tile=tile)
+            out = ds.out_f64()
+            compare(out, oracle_out(data, ds.shape.scale), label=f"edges{splits}/tile{tile}")
         # a row that sees one key returns that key's value exactly
         v0 = OA.bf16_to_f64(data.v_new[0])
         assert np.array_equal(out[0], np.repeat(v0, 8, axis=0))
 
 
-def test_tp_shard_shape(lib):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_tp_shard_shape(lib, tile):
     # one KV head with its 8 query heads: the shape of one tensor-parallel shard
     spec = I.random_small_step(5, max_seqs=4, max_n=50, max_c=200, n_q_heads=8, n_kv_heads=1)
-    data, ds = run_step(lib, spec, 5)
-    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label="tp-shard")
+    data, ds = run_step(lib, spec, 5, tile=tile)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"tp-shard/tile{tile}")
 
 
-def test_permuted_block_table_is_bit_identical(lib):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_permuted_block_table_is_bit_identical(lib, tile):
     spec = I.random_small_step(3, max_seqs=6, max_n=70, max_c=300)
-    _, a = run_step(lib, spec, 3, permute=True)
-    _, b = run_step(lib, spec, 3, permute=False)
+    _, a = run_step(lib, spec, 3, permute=True, tile=tile)
+    _, b = run_step(lib, spec, 3, permute=False, tile=tile)
     assert np.array_equal(a.out_f64(), b.out_f64())
 
 
-def test_deterministic_and_pool_contents_irrelevant(lib):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_deterministic_and_pool_contents_irrelevant(lib, tile):
     spec = I.config_small(0)
-    _, a = run_step(lib, spec, 2, pool_fill=SENTINEL)
-    _, b = run_step(lib, spec, 2, pool_fill=0)
+    _, a = run_step(lib, spec, 2, pool_fill=SENTINEL, tile=tile)
+    _, b = run_step(lib, spec, 2, pool_fill=0, tile=tile)
     ppas, step, torch = lib
     o1 = a.out_f64()
-    a.attend()
-    torch.cuda.synchronize()
+    ppas.set_tile_positions(tile)
+    try:
+        a.attend()
+        torch.cuda.synchronize()
+    finally:
+        ppas.set_tile_positions(0)
     assert np.array_equal(o1, a.out_f64())
     assert np.array_equal(o1, b.out_f64())
 
@@ -208,15 +222,16 @@ def sample_rows(spec, g, per_seq=12):
 
 
 @pytest.mark.parametrize("cfg", [2, 3, 4])
-def test_attention_full_size_sampled(lib, cfg):
+@pytest.mark.parametrize("tile", [16, 32])
+def test_attention_full_size_sampled(lib, cfg, tile):
     ppas, step, torch = lib
     spec = I.CONFIGS[cfg](0)
-    print(f"config {cfg} {spec.name}: rows={spec.n_rows}", flush=True)
-    data, ds = run_step(lib, spec, 0, spare=0)
+    print(f"config {cfg} {spec.name}: rows={spec.n_rows} tile={tile}", flush=True)
+    data, ds = run_step(lib, spec, 0, spare=0, tile=tile)
     rows = sample_rows(spec, I.rng(0, 77))
     ref = oracle_out(data, ds.shape.scale, rows=rows)
     out = ds.out_f64()
-    compare(out, ref, rows=rows, label=f"config{cfg} sampled {len(rows)} rows")
+    compare(out, ref, rows=rows, label=f"config{cfg} sampled {len(rows)} rows, tile {tile}")
     assert np.isfinite(out).all()
 
 
