@@ -373,6 +373,10 @@ def main():
             "attn_kernel_us": round(k_ms * 1e3, 2),
             "attn_kernel_us_min": round(float(np.min(attn_ms)) * 1e3, 2),
             "kv_append_us": round(float(np.mean(app_ms)) * 1e3, 2),
+            "tflops_in_kernel": round(F / (k_ms * 1e-3) / 1e12, 2),
+            "mfma_frac": round(F / (k_ms * 1e-3) / 1e12 / PEAK_TFLOPS, 4),
+            "kv_gbps_in_kernel": round(M.kv_bytes(spec) / (k_ms * 1e-3) / 1e9, 2),
+            "hbm_frac": round(M.kv_bytes(spec) / (k_ms * 1e-3) / 1e9 / PEAK_GBPS, 4),
             "prefill_tflops_in_kernel": round(M.flops(spec, "prefill") / (k_ms * 1e-3) / 1e12, 2),
             "decode_kv_gbps_in_kernel": round(M.kv_bytes(spec, "decode") / (k_ms * 1e-3) / 1e9, 2),
             "step_roofline_us": round(max(t_flop, t_byte) * 1e6, 2),
