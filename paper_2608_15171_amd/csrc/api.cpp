@@ -58,9 +58,10 @@ DeviceInfo current_device() {
   return d;
 }
 
-// Pinned host staging for the work-list upload. A slot is reused only after the
-// event recorded behind its copy has completed, so callers never wait on the
-// device unless kSlots uploads are still in flight.
+// Pinned host staging for the work-list upload, one ring per device (a slot's
+// completion event belongs to the device it was created on). A slot is reused
+// only after the event recorded behind its copy has completed, so callers never
+// wait on the device unless kSlots uploads are still in flight on it.
 constexpr int kSlots = 8;
 struct Slot {
   void* host = nullptr;
@@ -68,13 +69,20 @@ struct Slot {
   hipEvent_t done = nullptr;
   bool pending = false;
 };
-Slot g_slots[kSlots];
-int g_next = 0;
+struct Ring {
+  Slot slots[kSlots];
+  int next = 0;
+};
+std::vector<Ring> g_rings;
 
 ppas_status upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return PPAS_EHIP;
   std::lock_guard<std::mutex> lk(g_mu);
-  Slot& s = g_slots[g_next];
-  g_next = (g_next + 1) % kSlots;
+  if (dev >= int(g_rings.size())) g_rings.resize(size_t(dev) + 1);
+  Ring& ring = g_rings[size_t(dev)];
+  Slot& s = ring.slots[ring.next];
+  ring.next = (ring.next + 1) % kSlots;
   if (s.pending) {
     if (hipEventSynchronize(s.done) != hipSuccess) return PPAS_EHIP;
     s.pending = false;
