@@ -148,7 +148,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   int64_t ksp = g_prefill_split.load();
   if (ksp <= 0) {
     const int64_t target = int64_t(PPAS_PREFILL_ITEMS_PER_CU) * num_cus;
-    ksp = std::max<int64_t>(1024, ceil_div(prefill_keys, target));
+    ksp = std::max<int64_t>(256, ceil_div(prefill_keys, target));
   }
   ksp = std::max<int64_t>(kPrefillBlock, ceil_div(ksp, kPrefillBlock) * kPrefillBlock);
   int64_t ksd = g_decode_split.load();
