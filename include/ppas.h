@@ -114,9 +114,9 @@ ppas_status ppas_kv_append(const ppas_shape* shape, void* k_pages, void* v_pages
 
 /*
  * Device workspace that ppas_attn_step needs for this step description on the
- * current device: the work list plus fp32 partial results of rows whose keys are
- * split across workgroups. Depends only on the shape, the descriptors and the
- * device's compute-unit count. Returns 0 if the description is invalid.
+ * current device: fp32 partial results of rows whose keys are split across
+ * workgroups (at least 256 bytes). Depends only on the shape, the descriptors
+ * and the device's compute-unit count. Returns 0 if the description is invalid.
  */
 size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs);
 
@@ -134,8 +134,11 @@ size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, 
  * across workgroups are merged by a second, small launch.
  * workspace: device buffer of at least ppas_attn_workspace_bytes() bytes, owned
  * by the caller, not read before being written; it must not be used by another
- * call still in flight. Returns PPAS_OK, a validation status, PPAS_ENOSPACE or
- * PPAS_EHIP.
+ * call still in flight. The work list itself travels in pinned host memory the
+ * library owns (a ring of eight staging buffers per device, read by the kernels
+ * directly); a call waits on the device only when the buffer it would reuse is
+ * still being read by a launch eight calls back. Returns PPAS_OK, a validation
+ * status, PPAS_ENOSPACE or PPAS_EHIP.
  */
 ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q,
                            const void* k_pages, const void* v_pages,

@@ -58,13 +58,17 @@ DeviceInfo current_device() {
   return d;
 }
 
-// Pinned host staging for the work-list upload, one ring per device (a slot's
-// completion event belongs to the device it was created on). A slot is reused
-// only after the event recorded behind its copy has completed, so callers never
-// wait on the device unless kSlots uploads are still in flight on it.
+// Pinned host staging for the work list, one ring per device (a slot's
+// completion event belongs to the device it was created on). The kernels read
+// their items straight from the slot's pinned memory: each workgroup reads its
+// 32-byte item once, which costs less than a host-to-device copy on a separate
+// engine and the two cross-engine waits around it. A slot is refilled only after
+// the event recorded behind the last kernel that reads it has completed, so
+// callers wait on the device only when kSlots launches are still in flight.
 constexpr int kSlots = 8;
 struct Slot {
   void* host = nullptr;
+  char* dev = nullptr;      // the same memory as the device addresses it
   size_t cap = 0;
   hipEvent_t done = nullptr;
   bool pending = false;
@@ -74,11 +78,12 @@ struct Ring {
   int next = 0;
 };
 std::vector<Ring> g_rings;
+std::mutex g_stage_mu;     // held from taking a slot until its event is recorded
 
-ppas_status upload(const void* src, size_t bytes, void* dst, hipStream_t stream) {
+// The next slot of the current device's ring, with room for `bytes`. Caller holds g_stage_mu.
+ppas_status take_slot(size_t bytes, Slot*& out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return PPAS_EHIP;
-  std::lock_guard<std::mutex> lk(g_mu);
   if (dev >= int(g_rings.size())) g_rings.resize(size_t(dev) + 1);
   Ring& ring = g_rings[size_t(dev)];
   Slot& s = ring.slots[ring.next];
@@ -91,16 +96,21 @@ ppas_status upload(const void* src, size_t bytes, void* dst, hipStream_t stream)
   if (s.cap < bytes) {
     if (s.host) (void)hipHostFree(s.host);
     s.host = nullptr;
+    s.dev = nullptr;
     s.cap = 0;
     size_t cap = 1 << 16;
     while (cap < bytes) cap <<= 1;
     if (hipHostMalloc(&s.host, cap, hipHostMallocDefault) != hipSuccess) return PPAS_EHIP;
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, s.host, 0) != hipSuccess) {
+      (void)hipHostFree(s.host);
+      s.host = nullptr;
+      return PPAS_EHIP;
+    }
+    s.dev = static_cast<char*>(d);
     s.cap = cap;
   }
-  std::memcpy(s.host, src, bytes);
-  if (hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream) != hipSuccess) return PPAS_EHIP;
-  if (hipEventRecord(s.done, stream) != hipSuccess) return PPAS_EHIP;
-  s.pending = true;
+  out = &s;
   return PPAS_OK;
 }
 
@@ -226,21 +236,29 @@ ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q, co
     if (workspace_bytes < plan.total) return PPAS_ENOSPACE;
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     char* ws = static_cast<char*>(workspace);
-    // one contiguous upload: items, then combine items at their aligned offset
-    std::vector<char> host(plan.off_ml, 0);
-    std::memcpy(host.data() + plan.off_items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
-    if (!plan.combine.empty())
-      std::memcpy(host.data() + plan.off_combine, plan.combine.data(), plan.combine.size() * sizeof(CombineItem));
-    st = upload(host.data(), host.size(), ws, stream);
+    // The work list (items, then combine items at their aligned offset) goes into a
+    // pinned staging slot that the kernels read directly; the workspace holds the
+    // split partials.
+    std::lock_guard<std::mutex> lk(g_stage_mu);
+    Slot* slot = nullptr;
+    st = take_slot(plan.list_bytes, slot);
     if (st != PPAS_OK) return st;
+    char* host = static_cast<char*>(slot->host);
+    std::memcpy(host, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+    if (!plan.combine.empty())
+      std::memcpy(host + plan.off_combine, plan.combine.data(), plan.combine.size() * sizeof(CombineItem));
     const hipError_t e = launch_attn_step(
         static_cast<const uint16_t*>(q), static_cast<uint16_t*>(out), static_cast<const uint16_t*>(k_pages),
         static_cast<const uint16_t*>(v_pages), block_table_dev, bt_stride, shape->n_q_heads, shape->n_kv_heads,
-        shape->scale, reinterpret_cast<const WorkItem*>(ws + plan.off_items), int(plan.items.size()),
-        reinterpret_cast<const CombineItem*>(ws + plan.off_combine), int(plan.combine.size()),
+        shape->scale, reinterpret_cast<const WorkItem*>(slot->dev), int(plan.items.size()),
+        reinterpret_cast<const CombineItem*>(slot->dev + plan.off_combine), int(plan.combine.size()),
         reinterpret_cast<float2*>(ws + plan.off_ml), reinterpret_cast<float*>(ws + plan.off_acc), plan.tile_pos, stream,
         static_cast<hipEvent_t>(g_ev_start.load()), static_cast<hipEvent_t>(g_ev_stop.load()));
-    return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
+    // the slot is free again once the last kernel that reads it has finished (also
+    // after a failed launch: a kernel that did start may still read it)
+    const bool recorded = hipEventRecord(slot->done, stream) == hipSuccess;
+    slot->pending = recorded;
+    return (e == hipSuccess && recorded) ? PPAS_OK : PPAS_EHIP;
   } catch (...) {
     return PPAS_EINVAL;
   }

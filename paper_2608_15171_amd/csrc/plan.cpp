@@ -251,12 +251,11 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   }
   for (size_t b = full; b < n; ++b) plan.items[b] = jobs[b].item;
 
-  plan.off_items = 0;
   plan.off_combine = align_up(n * sizeof(WorkItem), 256);
-  plan.off_ml = align_up(plan.off_combine + plan.combine.size() * sizeof(CombineItem), 256);
-  plan.off_acc = align_up(plan.off_ml + size_t(plan.part_slots) * 8, 256);
-  plan.total = align_up(plan.off_acc + size_t(plan.part_slots) * kHeadDim * 4, 256);
-  if (plan.total == 0) plan.total = 256;
+  plan.list_bytes = plan.off_combine + plan.combine.size() * sizeof(CombineItem);
+  plan.off_ml = 0;
+  plan.off_acc = align_up(size_t(plan.part_slots) * 8, 256);
+  plan.total = std::max<size_t>(256, align_up(plan.off_acc + size_t(plan.part_slots) * kHeadDim * 4, 256));
 }
 
 }  // namespace ppas

@@ -46,8 +46,10 @@ struct Plan {
   std::vector<WorkItem> items;     // in launch order
   std::vector<CombineItem> combine;
   int64_t part_slots = 0;
-  // workspace layout (bytes)
-  size_t off_items = 0, off_combine = 0, off_ml = 0, off_acc = 0, total = 0;
+  // work list as the kernels read it (bytes): items from 0, combine items at off_combine
+  size_t off_combine = 0, list_bytes = 0;
+  // caller workspace layout (bytes): the split partials (max, sum) then accumulators
+  size_t off_ml = 0, off_acc = 0, total = 0;
 };
 
 ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,

@@ -145,13 +145,13 @@ void check_plan(const Step& st, const Plan& plan) {
     comb_slots += int64_t(c.nsplit) * c.npos * kGroup;
   }
   CHECK(comb_slots == plan.part_slots);
-  // workspace layout: ordered, aligned, large enough for every array
-  CHECK(plan.off_items == 0);
-  CHECK(plan.off_combine >= plan.off_items + plan.items.size() * sizeof(WorkItem));
-  CHECK(plan.off_ml >= plan.off_combine + plan.combine.size() * sizeof(CombineItem));
-  CHECK(plan.off_acc >= plan.off_ml + size_t(plan.part_slots) * 8);
+  // work-list and workspace layouts: ordered, aligned, large enough for every array
+  CHECK(plan.off_combine >= plan.items.size() * sizeof(WorkItem) && plan.off_combine % 256 == 0);
+  CHECK(plan.list_bytes == plan.off_combine + plan.combine.size() * sizeof(CombineItem));
+  CHECK(plan.off_ml == 0);
+  CHECK(plan.off_acc >= size_t(plan.part_slots) * 8 && plan.off_acc % 256 == 0);
   CHECK(plan.total >= plan.off_acc + size_t(plan.part_slots) * kHeadDim * 4);
-  CHECK(plan.off_combine % 256 == 0 && plan.off_ml % 256 == 0 && plan.off_acc % 256 == 0 && plan.total % 256 == 0);
+  CHECK(plan.total >= 256 && plan.total % 256 == 0);
 }
 
 void fuzz() {
