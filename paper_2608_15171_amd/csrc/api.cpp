@@ -58,6 +58,13 @@ DeviceInfo current_device() {
   return d;
 }
 
+// Work-item counts and partial-slot offsets travel as int32 (and the item count
+// sets the launch grid): a step too large for that is refused.
+bool plan_fits(const Plan& plan) {
+  return plan.items.size() <= size_t(INT32_MAX) && plan.combine.size() <= size_t(INT32_MAX) &&
+         plan.part_slots <= int64_t(INT32_MAX) - 64 * kGroup;
+}
+
 // Pinned host staging for the work list, one ring per device (a slot's
 // completion event belongs to the device it was created on). The kernels read
 // their items straight from the slot's pinned memory: each workgroup reads its
@@ -168,6 +175,7 @@ int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n
     if (st != PPAS_OK) return st;
     Plan plan;
     make_plan(*shape, seqs, n_seqs, num_cus, plan);
+    if (!plan_fits(plan)) return PPAS_ERANGE;
     const int32_t n = int32_t(plan.items.size());
     if (items_out) {
       for (int32_t i = 0; i < n && i < capacity; ++i) {
@@ -194,7 +202,7 @@ size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, 
     if (validate(shape, seqs, n_seqs, nullptr, INT32_MAX, false) != PPAS_OK) return 0;
     Plan plan;
     make_plan(*shape, seqs, n_seqs, current_device().cus, plan);
-    return plan.total;
+    return plan_fits(plan) ? plan.total : 0;
   } catch (...) {
     return 0;
   }
@@ -233,6 +241,7 @@ ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q, co
     if (!dev.gfx950) return PPAS_EUNSUPPORTED;
     Plan plan;
     make_plan(*shape, seqs, n_seqs, dev.cus, plan);
+    if (!plan_fits(plan)) return PPAS_ERANGE;
     if (workspace_bytes < plan.total) return PPAS_ENOSPACE;
     hipStream_t stream = static_cast<hipStream_t>(hip_stream);
     char* ws = static_cast<char*>(workspace);
