@@ -55,7 +55,8 @@ extern "C" {
 typedef enum ppas_status {
   PPAS_OK = 0,
   PPAS_EINVAL = -1,        /* malformed argument: null pointer, bad descriptor, bad stride */
-  PPAS_ERANGE = -2,        /* a block-table entry outside [0, num_pages), or a length overflow */
+  PPAS_ERANGE = -2,        /* a block-table entry outside [0, num_pages), a length overflow, or a step
+                               too large for the int32 work list */
   PPAS_ENOSPACE = -3,      /* workspace smaller than ppas_attn_workspace_bytes() */
   PPAS_EHIP = -4,          /* a HIP runtime call or kernel launch failed */
   PPAS_EUNSUPPORTED = -5   /* shape outside the compiled set, or no gfx950 device */

@@ -132,7 +132,7 @@ const char* ppas_status_string(ppas_status status) {
   switch (status) {
     case PPAS_OK: return "PPAS_OK";
     case PPAS_EINVAL: return "PPAS_EINVAL: invalid argument or step description";
-    case PPAS_ERANGE: return "PPAS_ERANGE: block-table entry or length out of range";
+    case PPAS_ERANGE: return "PPAS_ERANGE: block-table entry, length or step size out of range";
     case PPAS_ENOSPACE: return "PPAS_ENOSPACE: workspace too small";
     case PPAS_EHIP: return "PPAS_EHIP: HIP runtime error";
     case PPAS_EUNSUPPORTED: return "PPAS_EUNSUPPORTED: shape or device outside the compiled set";
