@@ -138,8 +138,10 @@ size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, 
  * call still in flight. The work list itself travels in pinned host memory the
  * library owns (a ring of eight staging buffers per device, read by the kernels
  * directly); a call waits on the device only when the buffer it would reuse is
- * still being read by a launch eight calls back. Returns PPAS_OK, a validation
- * status, PPAS_ENOSPACE or PPAS_EHIP.
+ * still being read by a launch eight calls back. Because the work list is staged
+ * per call, a call cannot be captured into a HIP graph and replayed. Calls from
+ * several threads or on several streams are safe (each with its own workspace).
+ * Returns PPAS_OK, a validation status, PPAS_ENOSPACE or PPAS_EHIP.
  */
 ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q,
                            const void* k_pages, const void* v_pages,

@@ -305,3 +305,28 @@ def test_long_contexts_sampled(lib, decode_split):
     out = ds.out_f64()
     assert np.isfinite(out).all()
     compare(out, ref, rows=rows, label=f"long contexts sampled {len(rows)} rows")
+
+
+def test_steps_on_two_streams(lib):
+    """Two different steps submitted alternately on two streams, each with its own workspace,
+    enough times to wrap the library's staging ring; both match the oracle."""
+    ppas, step, torch = lib
+    specs = [I.random_small_step(11, max_seqs=5, max_n=60, max_c=250), I.config_small(1)]
+    runs = []
+    for k, spec in enumerate(specs):
+        data = I.make_step_data(spec, 40 + k)
+        bt, npages = I.make_block_table(spec, 40 + k, spare_pages=2)
+        ds = step.DeviceStep(data, bt, npages, pool_fill=SENTINEL)
+        ds.fill_history()
+        ds.append()
+        runs.append((data, ds))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for it in range(12):
+        for (data, ds), st in zip(runs, streams):
+            with torch.cuda.stream(st):
+                ppas.attn_step(ds.shape, ds.out, ds.q, ds.k_pages, ds.v_pages, ds.desc, ds.bt, ds.workspace,
+                               ds.bt_host, stream=st.cuda_stream)
+    torch.cuda.synchronize()
+    for k, (data, ds) in enumerate(runs):
+        compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"stream {k}")
