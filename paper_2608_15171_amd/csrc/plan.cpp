@@ -177,9 +177,10 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
       Job j;
       j.item = WorkItem{s, g, row0, pos0, npos | (kind << 16), int32_t(lo), int32_t(hi),
                         part < 0 ? -1 : int32_t(part + k * int64_t(npos) * kGroup)};
-      // relative cost: a prefill key costs ~128 rows of MFMA work, a decode key
-      // ~512 bytes of HBM traffic; one decode key is about two prefill keys.
-      j.cost = double(hi - lo) * (kind == kKindDecode ? 2.0 : 1.0);
+      // relative cost: a prefill key of a 16-position tile costs 128 rows of MFMA
+      // work (twice that in a 32-position tile), a decode key ~512 bytes of HBM
+      // traffic; one decode key is about two prefill keys of a 16-position tile.
+      j.cost = double(hi - lo) * (kind == kKindDecode ? 2.0 : double(tile) / kTilePosSmall);
       j.order_key[0] = s;
       j.order_key[1] = g;
       j.order_key[2] = -pos0;
