@@ -18,7 +18,6 @@ CPU oracle on a bounded sample of the same step's rows.
 from __future__ import annotations
 
 import argparse
-import ctypes
 import json
 import math
 import os
@@ -57,31 +56,6 @@ def measured_traffic(workload: str):
     if rec.get("kernel_sources_sha256") != h.hexdigest():
         return None
     return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
-
-
-class HipEvents:
-    """hipEvent_t pairs through the HIP runtime (timing events on the launch stream)."""
-
-    def __init__(self):
-        self.hip = ctypes.CDLL("libamdhip64.so")
-        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
-        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
-        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
-
-    def create(self):
-        ev = ctypes.c_void_p()
-        if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
-            raise RuntimeError("hipEventCreate failed")
-        return ev.value
-
-    def elapsed_ms(self, a, b) -> float:
-        ms = ctypes.c_float()
-        if self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
-            raise RuntimeError("hipEventElapsedTime failed")
-        return ms.value
-
-    def destroy(self, ev):
-        self.hip.hipEventDestroy(ev)
 
 
 def cpu_baseline(data, scale, budget_s: float):
@@ -296,6 +270,7 @@ def main():
     pools = [(ds.k_pages, ds.v_pages)] + [(ds.k_pages.clone(), ds.v_pages.clone()) for _ in range(copies - 1)]
     torch.cuda.synchronize()
 
+    from paper_2608_15171_amd.hip_events import HipEvents
     hip = HipEvents()
     K, W = args.steps, args.warmup
     ev = [(hip.create(), hip.create()) for _ in range(K)]

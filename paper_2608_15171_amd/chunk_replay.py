@@ -21,7 +21,7 @@ import numpy as np
 from . import inputs as I
 from . import metrics as M
 from . import ppas
-from .trace_run import _Events
+from .hip_events import HipEvents
 
 _STREAM = 41   # seed stream kind of this module's inputs (distinct from inputs.py's kinds)
 
@@ -66,7 +66,7 @@ class Replay:
         self.v_pages = torch.zeros((pages, H, D, P), dtype=torch.bfloat16, device=device)
         self.out = torch.empty((prompt, I.HQ, D), dtype=torch.bfloat16, device=device)
         self.ws = torch.empty(256, dtype=torch.uint8, device=device)
-        self.events = _Events()
+        self.events = HipEvents()
 
     def run(self, chunk: int) -> list:
         """Prefill the whole prompt in chunks of `chunk` tokens; returns each chunk's
@@ -92,7 +92,7 @@ class Replay:
                 ppas.set_profile_events(None, None)
             evs.append((e0, e1))
         torch.cuda.synchronize()
-        ms = [self.events.ms(a, b) for a, b in evs]
+        ms = [self.events.elapsed_ms(a, b) for a, b in evs]
         for a, b in evs:
             self.events.destroy(a)
             self.events.destroy(b)

@@ -14,7 +14,6 @@ host for checking. Token content does not affect timing.
 """
 from __future__ import annotations
 
-import ctypes
 import math
 from dataclasses import dataclass
 
@@ -24,6 +23,7 @@ from . import inputs as I
 from . import metrics as M
 from . import ppas
 from . import ppas_trace as PT
+from .hip_events import HipEvents
 
 LAYER_SHIFT = 97
 
@@ -89,29 +89,6 @@ def logical_kv_rows(setup: TraceSetup, req_id: int, layer: int, length: int):
     return setup.base_kv[r] + LAYER_SHIFT * layer + np.arange(length)
 
 
-class _Events:
-    def __init__(self):
-        self.hip = ctypes.CDLL("libamdhip64.so")
-        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
-        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
-        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
-
-    def create(self):
-        ev = ctypes.c_void_p()
-        if self.hip.hipEventCreate(ctypes.byref(ev)) != 0:
-            raise RuntimeError("hipEventCreate failed")
-        return ev.value
-
-    def ms(self, a, b):
-        out = ctypes.c_float()
-        if self.hip.hipEventElapsedTime(ctypes.byref(out), a, b) != 0:
-            raise RuntimeError("hipEventElapsedTime failed")
-        return out.value
-
-    def destroy(self, e):
-        self.hip.hipEventDestroy(e)
-
-
 def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress=None):
     """Run every step of the trace in every layer. `check` lists (step index, layer)
     pairs whose outputs are copied back to the host. Returns a dict of timings and
@@ -124,7 +101,7 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     shape = ppas.make_shape(I.HQ, I.HKV, setup.num_pages)
     pools = [(torch.zeros((setup.num_pages, H, D // 8, P, 8), dtype=torch.bfloat16, device=device),
               torch.zeros((setup.num_pages, H, D, P), dtype=torch.bfloat16, device=device)) for _ in range(layers)]
-    ev = _Events()
+    ev = HipEvents()
     attn_events, app_events = [], []
     checks = {}
     want = set(check)
@@ -167,7 +144,7 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
             progress(si, len(setup.steps))
     t1.record()
     torch.cuda.synchronize()
-    attn_ms = [ev.ms(a, b) for a, b in attn_events]
+    attn_ms = [ev.elapsed_ms(a, b) for a, b in attn_events]
     app_ms = [a.elapsed_time(b) for a, b in app_events]
     for a, b in attn_events:
         ev.destroy(a)
