@@ -63,6 +63,9 @@ __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *reinterpret_
 __device__ __forceinline__ u32x4 ldg16_nt(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
+__device__ __forceinline__ u32x2 ldg8_nt(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+}
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -114,6 +117,20 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
     uint32_t m = 0;
     if (first + 2 * w < lim) m |= 0x0000ffffu;
     if (first + 2 * w + 1 < lim) m |= 0xffff0000u;
+    v[w] &= m;
+  }
+  return v;
+}
+
+// Two 4-element halves: zero elements e >= lim0 of the first and e >= lim1 of the second.
+__device__ __forceinline__ u32x4 keep_first_halves(u32x4 v, int lim0, int lim1) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const int lim = w < 2 ? lim0 : lim1;
+    const int e = 2 * (w & 1);
+    uint32_t m = 0;
+    if (e < lim) m |= 0x0000ffffu;
+    if (e + 1 < lim) m |= 0xffff0000u;
     v[w] &= m;
   }
   return v;
@@ -421,12 +438,14 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 // The W waves take interleaved 32-key blocks and stream K/V from HBM straight
 // into 16x16x32 MFMA operands (heads in the N dimension, padded 8 -> 16), then
 // merge their running (m, l, acc) through LDS.
-// Lane (n = lane & 15, q = lane >> 4): K rows of tile t are keys 8*(m/4) + 4t + m%4,
-// so after S^T lane q holds keys 8q..8q+7 of the block, which is exactly the k
-// range of its P^T operand slot; its V^T operand is the 16 contiguous bytes of
-// feature d holding keys 8q..8q+7. The QK^T reduction runs over features in the
-// order 32q + 8j + i (k-step j) for both the Q and K operands, so lane q's K
-// operand is chunks 4q..4q+3 of its key.
+// Lane (n = lane & 15, q = lane >> 4): S^T tile t is the block's page t (row m =
+// key 16t + m), so one K load reads whole 256-byte chunk runs of a page, and
+// after S^T lane q holds keys 4q..4q+3 of each page. The PV product takes its k
+// elements in that order: element 8q + 4t + i is key 16t + 4q + i, so the
+// probabilities stay in the lanes that computed them, and lane q's V^T operand
+// is the two 8-byte runs of feature d holding keys 4q..4q+3 of each page. The
+// QK^T reduction runs over features in the order 32q + 8j + i (k-step j) for
+// both the Q and K operands, so lane q's K operand is chunks 4q..4q+3 of its key.
 // ---------------------------------------------------------------------------
 template <int kW>
 __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it, char* smem) {
@@ -452,25 +471,26 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   const int nblk = (kend - it.key_lo + kDecodeBlock - 1) / kDecodeBlock;
   const int nmine = nblk > w ? (nblk - w + kWaves - 1) / kWaves : 0;   // blocks w, w+W, ... of this wave
 
-  const int krow = 8 * (n >> 2) + (n & 3);   // + 4t for tile t: key row of the K operand
-
   // Page ids. Item key ranges start on 32-key boundaries, so block b covers
   // pages first + 2b and first + 2b + 1. This wave's i-th block is b = w + Wi;
-  // lane L of a page-id register holds page 2(w + W(i0 + L/2)) + (L & 1) for the
-  // register's base block i0, so one register serves 32 blocks and the ids of a
-  // block come out with two lane reads, with no load on the loop's critical path.
+  // lane L of page-id register r holds page 2(w + W(32r + L/2)) + (L & 1), so one
+  // register serves 32 blocks and the ids of a block come out with two lane
+  // reads, with no load on the loop's critical path. Ids past the item's last
+  // page are clamped to it, so every block's loads stay inside the item's pages.
   const int first_page = it.key_lo >> 4;
   const int last_page = (kend - 1) >> 4;
-  auto load_pids = [&](int i0) {
-    const int blk = w + kWaves * (i0 + (lane >> 1));
-    return btrow[min(first_page + 2 * blk + (lane & 1), last_page)];
-  };
-  // The planner caps decode key ranges at kDecodeMaxKeys, so a wave has at most 64 blocks.
-  static_assert(kDecodeMaxKeys <= kWaves * 64 * kDecodeBlock, "two page-id registers per wave");
-  const int pid_lo = load_pids(0), pid_hi = load_pids(32);
+  constexpr int kPidRegs = kDecodeMaxKeys / (kWaves * 32 * kDecodeBlock);
+  static_assert(kPidRegs * kWaves * 32 * kDecodeBlock == kDecodeMaxKeys, "whole page-id registers");
+  int pid[kPidRegs];
+#pragma unroll
+  for (int r = 0; r < kPidRegs; ++r) {
+    const int blk = w + kWaves * (32 * r + (lane >> 1));
+    pid[r] = btrow[min(first_page + 2 * blk + (lane & 1), last_page)];
+  }
   // Complete the page-id loads here, once (the Q loads stay in flight), so the
   // loop never waits on them.
-  asm volatile("" ::"v"(pid_lo), "v"(pid_hi));
+#pragma unroll
+  for (int r = 0; r < kPidRegs; ++r) asm volatile("" ::"v"(pid[r]));
 
   // One 32-key block of this lane's MFMA operands: K rows for the two S^T tiles
   // and V^T chunks for the eight feature tiles. Two sets alternate so that the
@@ -479,64 +499,42 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     u32x4 k[2][4];
     u32x4 v[8];
   };
-  // K row keys krow + 4t lie in the block's second page iff n >= 8; V chunk keys
-  // 8q..8q+7 iff q >= 2.
-  const uint32_t k_lane = uint32_t(head_off) + 4 * q * kChunkElems;
-  const uint32_t v_lane = uint32_t(head_off) + n * kPage + 8 * (q & 1);
-  auto bases = [&](int i, const uint16_t*& kbase, const uint16_t*& vbase) {
-    const int l0 = __builtin_amdgcn_readlane(pid_lo, 2 * (i & 31));
-    const int l1 = __builtin_amdgcn_readlane(pid_lo, 2 * (i & 31) + 1);
-    const int h0 = __builtin_amdgcn_readlane(pid_hi, 2 * (i & 31));
-    const int h1 = __builtin_amdgcn_readlane(pid_hi, 2 * (i & 31) + 1);
-    const int p0 = (i < 32) ? l0 : h0;
-    const int p1 = (i < 32) ? l1 : h1;
-    kbase = a.kp + size_t(n >= 8 ? p1 : p0) * page_stride + k_lane;
-    vbase = a.vp + size_t(q >= 2 ? p1 : p0) * page_stride + v_lane;
-  };
-  // Full block: every key < kend.
-  auto gload = [&](Blk& B, int i) {
-    const uint16_t *kbase, *vbase;
-    bases(i, kbase, vbase);
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const uint16_t* src = kbase + ((krow + 4 * t) & 15) * 8;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t) B.v[t] = ldg16_nt(vbase + 16 * t * kPage);
-  };
-  // Ragged last block: keys >= kend load nothing and stay zero.
-  auto gload_tail = [&](Blk& B, int i, int kb) {
-    const uint16_t *kbase, *vbase;
-    bases(i, kbase, vbase);
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int key = kb + krow + 4 * t;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) B.k[t][j] = u32x4{0, 0, 0, 0};
-      if (key < kend) {
-        const uint16_t* src = kbase + ((krow + 4 * t) & 15) * 8;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) B.k[t][j] = ldg16_nt(src + j * kChunkElems);
-      }
-    }
-    const int key0 = kb + 8 * q;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) B.v[t] = u32x4{0, 0, 0, 0};
-    if (key0 < kend) {
-      const int lim = kend - key0;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) B.v[t] = keep_first(ldg16(vbase + 16 * t * kPage), 0, lim);
-    }
-  };
-  // wave-block i = global block w + W i
+  // K: chunk 4q + j, slot n of page t; V: feature 16tt + n, slots 4q..4q+3 of each page
+  const uint32_t k_lane = uint32_t(head_off) + 4 * q * kChunkElems + 8 * n;
+  const uint32_t v_lane = uint32_t(head_off) + n * kPage + 4 * q;
+  // Every load() issues exactly the same 24 loads, with no branch around
+  // any of them (a ragged last block reads clamped pages and is masked where it
+  // is consumed). The count of loads in flight is then the same on every path
+  // into consume(), so each of its waits lets the next block's loads stay
+  // outstanding.
   auto load = [&](Blk& B, int i) {
-    const int kb = it.key_lo + (w + kWaves * i) * kDecodeBlock;
-    if (kb + kDecodeBlock <= kend)
-      gload(B, i);
-    else
-      gload_tail(B, i, kb);
+    // lane reads from every register, then a scalar choice (a register chosen by
+    // a runtime index would be moved to memory)
+    const int r = i >> 5, l0 = 2 * (i & 31);
+    int p0 = __builtin_amdgcn_readlane(pid[0], l0);
+    int p1 = __builtin_amdgcn_readlane(pid[0], l0 + 1);
+#pragma unroll
+    for (int k = 1; k < kPidRegs; ++k) {
+      const int c0 = __builtin_amdgcn_readlane(pid[k], l0);
+      const int c1 = __builtin_amdgcn_readlane(pid[k], l0 + 1);
+      p0 = (r == k) ? c0 : p0;
+      p1 = (r == k) ? c1 : p1;
+    }
+    const uint16_t* k0 = a.kp + size_t(p0) * page_stride + k_lane;
+    const uint16_t* k1 = a.kp + size_t(p1) * page_stride + k_lane;
+    const uint16_t* v0 = a.vp + size_t(p0) * page_stride + v_lane;
+    const uint16_t* v1 = a.vp + size_t(p1) * page_stride + v_lane;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      B.k[0][j] = ldg16_nt(k0 + j * kChunkElems);
+      B.k[1][j] = ldg16_nt(k1 + j * kChunkElems);
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const u32x2 lo = ldg8_nt(v0 + 16 * t * kPage);
+      const u32x2 hi = ldg8_nt(v1 + 16 * t * kPage);
+      B.v[t] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
   };
 
   f32x4 oacc[8];
@@ -544,7 +542,10 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
   for (int t = 0; t < 8; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
 
+  // Block at keys kb..kb+31. In a ragged last block, keys >= kend get logit
+  // -inf and zero V, whatever their (clamped) pages hold.
   auto consume = [&](const Blk& B, int kb) {
+    const bool tail = kb + kDecodeBlock > kend;
     f32x4 sacc[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -553,13 +554,13 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
       for (int j = 0; j < 4; ++j)
         sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.k[t][j]), qf[j], sacc[t], 0, 0, 0);
     }
-    // S^T register r of tile t: key kb + 8q + 4t + r
-    if (kb + kDecodeBlock > kend) {
+    // S^T register r of tile t: key kb + 16t + 4q + r
+    if (tail) {
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (kb + 8 * q + 4 * t + r >= kend) sacc[t][r] = kNegInf;
+          if (kb + 16 * t + 4 * q + r >= kend) sacc[t][r] = kNegInf;
     }
     float mx = kNegInf;
 #pragma unroll
@@ -582,23 +583,36 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
         lsum = sum_bf16x2(pr, lsum);
       }
     l_run += lsum;
+    // V^T halves: keys kb + 4q .. +3 and kb + 16 + 4q .. +3
+    const int vlim0 = kend - (kb + 4 * q), vlim1 = kend - (kb + 16 + 4 * q);
 #pragma unroll
-    for (int t = 0; t < 8; ++t)
-      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(B.v[t]), as_bf16x8(pb), oacc[t], 0, 0, 0);
+    for (int t = 0; t < 8; ++t) {
+      const u32x4 vv = tail ? keep_first_halves(B.v[t], vlim0, vlim1) : B.v[t];
+      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), as_bf16x8(pb), oacc[t], 0, 0, 0);
+    }
   };
 
-  // wave w takes blocks w, w+W, w+2W, ... (wave-block i = block w + W i)
-  Blk A, B;
-  int i = 0;
-  if (i < nmine) load(A, i);
-  while (i < nmine) {
-    if (i + 1 < nmine) load(B, i + 1);
-    consume(A, it.key_lo + (w + kWaves * i) * kDecodeBlock);
-    ++i;
-    if (i >= nmine) break;
-    if (i + 1 < nmine) load(A, i + 1);
-    consume(B, it.key_lo + (w + kWaves * i) * kDecodeBlock);
-    ++i;
+  // wave w takes blocks w, w+W, w+2W, ... (wave-block i = block w + W i). The
+  // block after the last one is loaded as a (clamped, unused) copy of the last,
+  // so the loop body always issues its loads.
+  if (nmine > 0) {
+    Blk A, B;
+    const int last = nmine - 1;
+    auto kb_of = [&](int i) { return it.key_lo + (w + kWaves * i) * kDecodeBlock; };
+    // the scheduling barriers keep each block's loads ahead of the previous
+    // block's arithmetic, so two blocks are in flight while one is consumed
+    load(A, 0);
+    for (int i = 0;; i += 2) {
+      load(B, min(i + 1, last));
+      __builtin_amdgcn_sched_barrier(0);
+      consume(A, kb_of(i));
+      if (i + 1 > last) break;
+      load(A, min(i + 2, last));
+      __builtin_amdgcn_sched_barrier(0);
+      consume(B, kb_of(i + 1));
+      if (i + 2 > last) break;
+    }
+    wait_vmem();
   }
 
   // Merge the waves. O^T register r of feature tile t holds feature 16t + 4q + r.

@@ -19,7 +19,7 @@ constexpr int kTilePosSmall = 16;
 constexpr int kTilePosLarge = 32;
 constexpr int kPrefillBlock = 64;  // keys per staged K/V block of a prefill tile
 constexpr int kDecodeBlock = 32;   // keys per block of a decode wave
-constexpr int kDecodeMaxKeys = 8192;  // longest key range of one decode item
+constexpr int kDecodeMaxKeys = 16384;  // longest key range of one decode item
 constexpr int kKindPrefill = 0;
 constexpr int kKindDecode = 1;
 

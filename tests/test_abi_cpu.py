@@ -179,9 +179,10 @@ def test_plan_is_deterministic():
 
 @pytest.mark.parametrize("decode_split", [0, 8192, 1 << 20])
 def test_decode_items_never_exceed_the_page_id_capacity(decode_split):
-    """A decode work item holds the page ids of its blocks in two lane registers per wave
-    (64 blocks of 32 keys per wave, four waves): its key range is capped at 8,192 keys,
-    also when a larger split is requested."""
+    """A decode work item holds the page ids of its blocks in lane registers (32 blocks of
+    32 keys per register; four registers per wave of the four-wave kernel, two per wave of
+    the eight-wave one): its key range is capped at 16,384 keys, also when a larger split
+    is requested."""
     spec = I.StepSpec("long-decodes", [I.Seq(1, c, i) for i, c in enumerate([0, 8191, 8192, 60000, 300000])])
     ppas.set_split_keys(0, decode_split)
     try:
@@ -189,6 +190,6 @@ def test_decode_items_never_exceed_the_page_id_capacity(decode_split):
     finally:
         ppas.set_split_keys(0, 0)
     dec = items[items[:, 0] == 1]
-    assert (dec[:, 7] - dec[:, 6]).max() <= 8192
+    assert (dec[:, 7] - dec[:, 6]).max() <= 16384
     assert (dec[:, 6] % 32 == 0).all(), "decode key ranges start on 32-key blocks"
     check_coverage(spec, items)
