@@ -159,12 +159,40 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   ksd = std::max<int64_t>(kDecodeBlock, ceil_div(ksd, kDecodeBlock) * kDecodeBlock);
   ksd = std::min<int64_t>(ksd, kDecodeMaxKeys);
 
+  // Prefill tiles load the matrix cores and decode items the memory system. When
+  // the decode work is comparable to the prefill work, the two kinds are
+  // interleaved in the launch order (below); otherwise decode goes last.
+  const double tile_cost = double(tile) / kTilePosSmall;   // per key, relative to a 16-position tile
+  const bool interleave = 2.0 * double(decode_keys) >= kInterleaveRatio * tile_cost * double(prefill_keys);
+
+  // Key ranges of one tile or decode row. Decode rows, and prefill tiles of
+  // interleaved steps, take pieces of `split` keys from key 0 (the last one
+  // ragged: the short pieces fill the gaps between long items). Other prefill
+  // tiles take round(keys / split) even pieces, so a step's items come close to
+  // a whole number per workgroup slot. Prefill boundaries are multiples of the
+  // 64-key block at or before the tile's first position, so every row sees a
+  // key in every piece.
+  auto piece_bounds = [&](int64_t kend, int64_t pos0, int kind) {
+    std::vector<int64_t> b{0};
+    if (kind == kKindDecode) {
+      for (int64_t k = 1; k * ksd < kend; ++k) b.push_back(k * ksd);
+    } else if (interleave) {
+      for (int64_t k = 1; k * ksp <= pos0; ++k) b.push_back(k * ksp);
+    } else {
+      const int64_t n = std::max<int64_t>(1, (kend + ksp / 2) / ksp);
+      const int64_t top = pos0 / kPrefillBlock * kPrefillBlock;
+      for (int64_t k = 1; k < n; ++k) b.push_back(std::min(top, kend * k / n / kPrefillBlock * kPrefillBlock));
+    }
+    b.push_back(kend);
+    b.erase(std::unique(b.begin(), b.end()), b.end());
+    return b;
+  };
+
   std::vector<Job> jobs;
   auto add_unit = [&](int32_t s, int32_t g, int32_t row0, int32_t pos0, int32_t npos, int kind) {
     const int64_t kend = int64_t(pos0) + npos;        // keys 0..kend-1 are visible to some row
-    int64_t split = kind == kKindDecode ? ksd : ksp;
-    // prefill splits all start at or before pos0, so every row sees a key in every split
-    int64_t nsplit = kind == kKindDecode ? ceil_div(kend, split) : (int64_t(pos0) / split + 1);
+    const std::vector<int64_t> bounds = piece_bounds(kend, pos0, kind);
+    const int64_t nsplit = int64_t(bounds.size()) - 1;
     int32_t part = -1;
     if (nsplit > 1) {
       part = int32_t(plan.part_slots);
@@ -172,15 +200,14 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
       plan.part_slots += nsplit * int64_t(npos) * kGroup;
     }
     for (int64_t k = 0; k < nsplit; ++k) {
-      const int64_t lo = k * split;
-      const int64_t hi = (k + 1 == nsplit) ? kend : std::min(kend, (k + 1) * split);
+      const int64_t lo = bounds[size_t(k)], hi = bounds[size_t(k) + 1];
       Job j;
       j.item = WorkItem{s, g, row0, pos0, npos | (kind << 16), int32_t(lo), int32_t(hi),
                         part < 0 ? -1 : int32_t(part + k * int64_t(npos) * kGroup)};
       // relative cost: a prefill key of a 16-position tile costs 128 rows of MFMA
       // work (twice that in a 32-position tile), a decode key ~512 bytes of HBM
       // traffic; one decode key is about two prefill keys of a 16-position tile.
-      j.cost = double(hi - lo) * (kind == kKindDecode ? 2.0 : double(tile) / kTilePosSmall);
+      j.cost = double(hi - lo) * (kind == kKindDecode ? 2.0 : tile_cost);
       j.order_key[0] = s;
       j.order_key[1] = g;
       j.order_key[2] = -pos0;
@@ -214,15 +241,13 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   for (const Job& j : jobs) ((j.item.npos_kind >> 16) == kKindDecode ? dec : pre).push_back(j);
   std::stable_sort(pre.begin(), pre.end(), lpt);
   std::stable_sort(dec.begin(), dec.end(), lpt);
-  // Prefill tiles load the matrix cores and decode items the memory system. When
-  // the decode work is comparable to the prefill work, they run best side by
-  // side: merge the two queues so that both advance at the same fraction of
-  // their total work and finish together. When decode is a small share, it goes
-  // last and fills the tail of the prefill rounds.
+  // Interleaved steps merge the two queues so that both advance at the same
+  // fraction of their total work and finish together (prefill tiles load the
+  // matrix cores, decode items the memory system); otherwise decode goes last
+  // and fills the tail of the prefill rounds.
   double tot_p = 0, tot_d = 0;
   for (const Job& j : pre) tot_p += j.cost;
   for (const Job& j : dec) tot_d += j.cost;
-  const bool interleave = tot_d >= kInterleaveRatio * tot_p;
   jobs.clear();
   size_t ip = 0, id = 0;
   double done_p = 0, done_d = 0;

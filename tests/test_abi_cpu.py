@@ -164,10 +164,22 @@ def test_plan_covers_workloads(cfg):
     items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
     if cfg in (1, 2):
         check_coverage(spec, items)
-    # longest-first: the first launch slots hold the most keys on average
-    span = items[:, 7] - items[:, 6]
-    k = max(1, len(items) // 8)
-    assert span[:k].mean() >= span[-k:].mean()
+    # longest first within each kind: the first eighth of a kind's items holds at
+    # least as many keys on average as its last eighth
+    for kind in (0, 1):
+        span = (items[:, 7] - items[:, 6])[items[:, 0] == kind]
+        if len(span):
+            k = max(1, len(span) // 8)
+            assert span[:k].mean() >= span[-k:].mean()
+    dec_at = np.flatnonzero(items[:, 0] == 1)
+    if cfg in (1, 4):
+        # decode work comparable to the prefill work: the kinds are interleaved,
+        # each advancing through the launch at about the same fraction of its work
+        assert 0 < len(dec_at) < len(items)
+        assert dec_at.min() < len(items) // 4 and dec_at.max() >= len(items) * 3 // 4
+    elif len(dec_at):
+        # decode a small share of the step: decode items fill the tail
+        assert np.array_equal(dec_at, np.arange(len(items) - len(dec_at), len(items)))
 
 
 def test_plan_is_deterministic():
