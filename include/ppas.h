@@ -183,11 +183,12 @@ ppas_status ppas_set_tile_positions(int32_t tile_positions);
 
 /*
  * Profiling hook (process-wide). When both are non-NULL, the next
- * ppas_attn_step calls record `start_event` on their stream immediately before
- * the packed attention kernel is launched and `stop_event` immediately after it
- * (hipEvent_t handles created by the caller), so the kernel's own duration can
- * be read with hipEventElapsedTime. Pass NULLs to stop recording. The events are
- * re-recorded by every call; the caller owns and destroys them.
+ * ppas_attn_step calls have the packed attention kernel's launch record
+ * `start_event` when the kernel starts and `stop_event` when it ends
+ * (hipEvent_t handles created by the caller; hipExtLaunchKernel's events), so
+ * the kernel's own duration can be read with hipEventElapsedTime. Pass NULLs to
+ * stop recording. The events are re-recorded by every call; the caller owns and
+ * destroys them.
  * Returns PPAS_EINVAL if exactly one of them is NULL.
  */
 ppas_status ppas_set_profile_events(void* start_event, void* stop_event);

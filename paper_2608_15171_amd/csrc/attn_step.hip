@@ -11,6 +11,7 @@
 //
 // Page layouts: K pages are chunk-major, [16 chunks of 8 features][16 slots][8];
 // V pages are feature-major, [128 features][16 slots].
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -729,14 +730,17 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
     a.hq = hq;
     a.hkv = hkv;
     a.scale_log2 = scale * 1.4426950408889634f;
-    if (ev_start && hipEventRecord(ev_start, stream) != hipSuccess) return hipGetLastError();
+    // With profiling events, the launch itself records them at the dispatch's
+    // start and end (events recorded as separate commands would also time the
+    // gap between those commands and the dispatch).
     if (tile_pos == kTilePosLarge)
-      hipLaunchKernelGGL(attn_step_kernel<8>, dim3(n_items), dim3(threads_of<8>()), 0, stream, a);
+      hipExtLaunchKernelGGL(attn_step_kernel<8>, dim3(n_items), dim3(threads_of<8>()), 0, stream, ev_start, ev_stop,
+                            0, a);
     else
-      hipLaunchKernelGGL(attn_step_kernel<4>, dim3(n_items), dim3(threads_of<4>()), 0, stream, a);
+      hipExtLaunchKernelGGL(attn_step_kernel<4>, dim3(n_items), dim3(threads_of<4>()), 0, stream, ev_start, ev_stop,
+                            0, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess) return hipGetLastError();
   }
   if (n_comb > 0) {
     const int ymax = tile_pos * kGroup / kCombineRowsPerBlock;
