@@ -64,9 +64,6 @@ __device__ __forceinline__ u32x4 ldg16(const uint16_t* p) { return *reinterpret_
 __device__ __forceinline__ u32x4 ldg16_nt(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
-__device__ __forceinline__ u32x2 ldg8_nt(const uint16_t* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
-}
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -118,20 +115,6 @@ __device__ __forceinline__ u32x4 keep_first(u32x4 v, int first, int lim) {
     uint32_t m = 0;
     if (first + 2 * w < lim) m |= 0x0000ffffu;
     if (first + 2 * w + 1 < lim) m |= 0xffff0000u;
-    v[w] &= m;
-  }
-  return v;
-}
-
-// Two 4-element halves: zero elements e >= lim0 of the first and e >= lim1 of the second.
-__device__ __forceinline__ u32x4 keep_first_halves(u32x4 v, int lim0, int lim1) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const int lim = w < 2 ? lim0 : lim1;
-    const int e = 2 * (w & 1);
-    uint32_t m = 0;
-    if (e < lim) m |= 0x0000ffffu;
-    if (e + 1 < lim) m |= 0xffff0000u;
     v[w] &= m;
   }
   return v;
@@ -442,11 +425,12 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
 // Lane (n = lane & 15, q = lane >> 4): S^T tile t is the block's page t (row m =
 // key 16t + m), so one K load reads whole 256-byte chunk runs of a page, and
 // after S^T lane q holds keys 4q..4q+3 of each page. The PV product takes its k
-// elements in that order: element 8q + 4t + i is key 16t + 4q + i, so the
-// probabilities stay in the lanes that computed them, and lane q's V^T operand
-// is the two 8-byte runs of feature d holding keys 4q..4q+3 of each page. The
-// QK^T reduction runs over features in the order 32q + 8j + i (k-step j) for
-// both the Q and K operands, so lane q's K operand is chunks 4q..4q+3 of its key.
+// elements in key order (lane q: keys 8q..8q+7), so that lane q's V^T operand
+// is the 16 contiguous bytes of feature d holding those keys; the bf16
+// probabilities are regrouped into that order through a 1 KB LDS slot of the
+// wave. The QK^T reduction runs over features in the order 32q + 8j + i (k-step
+// j) for both the Q and K operands, so lane q's K operand is chunks 4q..4q+3 of
+// its key.
 // ---------------------------------------------------------------------------
 template <int kW>
 __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it, char* smem) {
@@ -500,10 +484,10 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     u32x4 k[2][4];
     u32x4 v[8];
   };
-  // K: chunk 4q + j, slot n of page t; V: feature 16tt + n, slots 4q..4q+3 of each page
+  // K: chunk 4q + j, slot n of page t; V: feature 16tt + n, slots 8(q & 1)..+7 of page q >> 1
   const uint32_t k_lane = uint32_t(head_off) + 4 * q * kChunkElems + 8 * n;
-  const uint32_t v_lane = uint32_t(head_off) + n * kPage + 4 * q;
-  // Every load() issues exactly the same 24 loads, with no branch around
+  const uint32_t v_lane = uint32_t(head_off) + n * kPage + 8 * (q & 1);
+  // Every load() issues exactly the same 16 loads, with no branch around
   // any of them (a ragged last block reads clamped pages and is masked where it
   // is consumed). The count of loads in flight is then the same on every path
   // into consume(), so each of its waits lets the next block's loads stay
@@ -523,25 +507,23 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
     }
     const uint16_t* k0 = a.kp + size_t(p0) * page_stride + k_lane;
     const uint16_t* k1 = a.kp + size_t(p1) * page_stride + k_lane;
-    const uint16_t* v0 = a.vp + size_t(p0) * page_stride + v_lane;
-    const uint16_t* v1 = a.vp + size_t(p1) * page_stride + v_lane;
+    const uint16_t* vb = a.vp + size_t(q >= 2 ? p1 : p0) * page_stride + v_lane;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       B.k[0][j] = ldg16_nt(k0 + j * kChunkElems);
       B.k[1][j] = ldg16_nt(k1 + j * kChunkElems);
     }
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const u32x2 lo = ldg8_nt(v0 + 16 * t * kPage);
-      const u32x2 hi = ldg8_nt(v1 + 16 * t * kPage);
-      B.v[t] = u32x4{lo[0], lo[1], hi[0], hi[1]};
-    }
+    for (int t = 0; t < 8; ++t) B.v[t] = ldg16_nt(vb + 16 * t * kPage);
   };
 
   f32x4 oacc[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
+  // this wave's probability-regrouping slot, past the region the final merge uses
+  char* pslot = smem + 3 * kBlockBytes + w * 1024;
+  static_assert(kWaves * 1024 <= kBlockBytes, "regrouping slots fit in the last ring block");
 
   // Block at keys kb..kb+31. In a ragged last block, keys >= kend get logit
   // -inf and zero V, whatever their (clamped) pages hold.
@@ -584,11 +566,17 @@ __device__ __forceinline__ void decode_row(const StepArgs& a, const WorkItem& it
         lsum = sum_bf16x2(pr, lsum);
       }
     l_run += lsum;
-    // V^T halves: keys kb + 4q .. +3 and kb + 16 + 4q .. +3
-    const int vlim0 = kend - (kb + 4 * q), vlim1 = kend - (kb + 16 + 4 * q);
+    // Regroup: the 8 bytes of (page t, keys 4q..4q+3) go to slot (n, t, q); lane q
+    // then reads keys 8q..8q+7 = (page q >> 1, quads 2(q & 1), 2(q & 1) + 1) as one
+    // 16-byte run.
+    *reinterpret_cast<u32x2*>(pslot + ((2 * n) * 4 + q) * 8) = u32x2{pb[0], pb[1]};
+    *reinterpret_cast<u32x2*>(pslot + ((2 * n + 1) * 4 + q) * 8) = u32x2{pb[2], pb[3]};
+    pb = lds16(pslot + ((2 * n + (q >> 1)) * 4 + 2 * (q & 1)) * 8);
+    // V^T chunk: keys kb + 8q .. +7
+    const int vlim = kend - (kb + 8 * q);
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      const u32x4 vv = tail ? keep_first_halves(B.v[t], vlim0, vlim1) : B.v[t];
+      const u32x4 vv = tail ? keep_first(B.v[t], 0, vlim) : B.v[t];
       oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vv), as_bf16x8(pb), oacc[t], 0, 0, 0);
     }
   };
