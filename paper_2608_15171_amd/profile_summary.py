@@ -79,7 +79,7 @@ def main(workload: str, d: str, calib: str):
         lines.append(f"| {r['Name'][:60]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {100 * float(r['TotalDurationNs']) / total:.1f}% |")
     a = attn[0]
-    lines += ["", f"bench.py in the same run, HIP events around the launch: {bench['roofline']['kernel_us']:.2f} us per "
+    lines += ["", f"bench.py in the same run, HIP events recorded by the launch: {bench['roofline']['kernel_us']:.2f} us per "
                   f"launch over its {bench['steps']} timed steps (rocprofv3 average {float(a['AverageNs']) / 1e3:.2f} us "
                   f"over {a['Calls']} launches including warm-up).", "",
               "## HBM traffic (rocprofv3 --pmc, one counter per run)", "", "Commands:", ""]
