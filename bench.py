@@ -101,6 +101,27 @@ def cpu_baseline(data, scale, budget_s: float):
     return rec, rows, ref
 
 
+def warm_up(step, args):
+    """Untimed warm-up. With --warmup N >= 0, exactly N steps; by default, steps until
+    --warmup-seconds of wall time have passed (at least 5 steps). The GPU raises its
+    clocks over the first ~50 ms of sustained work after idling, so a warm-up of a few
+    short steps would time that ramp instead of the kernel. Returns the step count."""
+    import torch
+    if args.warmup >= 0:
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        return args.warmup
+    n, t0 = 0, time.perf_counter()
+    while True:
+        for _ in range(5):
+            step(n)
+            n += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= args.warmup_seconds:
+            return n
+
+
 def parity_summary(out, ref, rows):
     """Max and mean |GPU - oracle| over the oracle's sample rows of the timed step."""
     import numpy as np
@@ -174,9 +195,10 @@ def run_chunks_workload(args):
     rp = CR.Replay(P, args.seed)
     n_chunks = P // C
     print(f"chunks: prompt {P} as {n_chunks} x {C} and as 1 x {P}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
+    def pair(_):
         rp.run(C)
         rp.run(P)
+    n_warm = warm_up(pair, args)
     chunked, single = [], []
     for _ in range(args.steps):
         chunked.append(rp.run(C))
@@ -192,7 +214,7 @@ def run_chunks_workload(args):
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": n_warm,
         "ms_per_step": round(t_single, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -229,7 +251,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed warm-up steps; default: as many as fill --warmup-seconds")
+    ap.add_argument("--warmup-seconds", type=float, default=0.25)
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mbt2048")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -288,9 +312,7 @@ def main():
         if timed:
             ppas.set_profile_events(None, None)
 
-    for i in range(W):
-        one_step(i, False)
-    torch.cuda.synchronize()
+    W = warm_up(lambda i: one_step(i, False), args)
     t0 = time.perf_counter()
     for i in range(K):
         one_step(i, True)
