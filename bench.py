@@ -27,6 +27,8 @@ import time
 WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              # diagnostics: parts of the pressure step alone
              "pressure-decode": "pressure-decode", "pressure-prefill": "pressure-prefill",
+             # one GPU's shard of the MBT=2048 and pressure steps split two ways by KV head
+             "mbt2048-tp2shard": "mbt2048-tp2shard", "pressure-tp2shard": "pressure-tp2shard",
              # 36-layer P-PAS serving trace (64 requests)
              "trace": None,
              # one prompt prefilled as several chunks vs as one chunk
@@ -357,7 +359,7 @@ def main():
                         f"{[(s.n_query, s.cached_len) for s in spec.seqs if s.n_query > 1]} (n_query, cached_len) chunks",
             "query_rows": spec.n_rows,
             "kv_tokens": int(spec.kv_lens().sum()),
-            "heads": "16q/2kv", "head_dim": 128, "page_size": 16, "block_table": "seeded permutation",
+            "heads": f"{spec.n_q_heads}q/{spec.n_kv_heads}kv", "head_dim": 128, "page_size": 16, "block_table": "seeded permutation",
             "kv_pool_copies_rotated": copies,
         },
         "roofline": {

@@ -11,4 +11,5 @@ Modules:
   attention -- the attention of a mixed step (chunked prefill rows and decode rows)
   kv_cache  -- where kv_append puts a step's new keys and values in the page pools
   policy    -- the P-PAS per-iteration prefill budget (Algorithm 1)
+  rope      -- rotary position embedding of a step's new Q and K rows before the append
 """

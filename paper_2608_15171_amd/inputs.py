@@ -131,6 +131,24 @@ def config_pressure_prefill_only(seed: int = 0) -> StepSpec:
     return StepSpec("pressure-2x1024-only", [s for s in full.seqs if s.n_query > 1])
 
 
+def tp2_shard(spec: StepSpec) -> StepSpec:
+    """One GPU's half of a step split two ways by KV head: query heads 8k..8k+7 and
+    KV head k (8 query heads, 1 KV head, the same requests and lengths)."""
+    return StepSpec(spec.name + "-tp2shard", spec.seqs, n_q_heads=spec.n_q_heads // 2,
+                    n_kv_heads=spec.n_kv_heads // 2, head_dim=spec.head_dim, page_size=spec.page_size,
+                    info=dict(spec.info))
+
+
+def config_small_budget_tp2(seed: int = 0) -> StepSpec:
+    """Diagnostic: the KV-head-split shard of the MBT=2048 step."""
+    return tp2_shard(config_small_budget(seed))
+
+
+def config_high_pressure_tp2(seed: int = 0) -> StepSpec:
+    """Diagnostic: the KV-head-split shard of the high-pressure step."""
+    return tp2_shard(config_high_pressure(seed))
+
+
 CONFIGS = {
     1: config_small,
     2: config_small_budget,
@@ -141,6 +159,8 @@ CONFIGS = {
 DIAGNOSTICS = {
     "pressure-decode": config_pressure_decode_only,
     "pressure-prefill": config_pressure_prefill_only,
+    "mbt2048-tp2shard": config_small_budget_tp2,
+    "pressure-tp2shard": config_high_pressure_tp2,
 }
 
 
