@@ -33,6 +33,21 @@ def bf16_bits_to_f64(x) -> np.ndarray:
     return (np.asarray(x, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def f64_to_bf16_bits(x) -> np.ndarray:
+    """float64 values to bf16 bit patterns, rounded to nearest, ties to even, in one
+    step: scale each value so its bf16 grid (8 significant bits) becomes the integers,
+    round with numpy's round-half-even, scale back (all exact in float64; values stay
+    in bf16's normal range here). The result is exactly representable in float32, whose
+    top 16 bits are the bf16 pattern."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros(x.shape, dtype=np.float64)
+    nz = x != 0
+    e = np.floor(np.log2(np.abs(x[nz])))
+    u = np.exp2(e - 7)                                   # grid spacing of the value's binade
+    out[nz] = np.rint(x[nz] / u) * u
+    return (out.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
 def angles(positions, head_dim: int, theta: float) -> np.ndarray:
     """[n, D/2] rotation angles: position p times theta^(-2i/D) for pair i."""
     pos = np.asarray(positions, dtype=np.float64)

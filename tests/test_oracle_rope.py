@@ -126,3 +126,24 @@ def test_append_after_rotation_copies_v_and_leaves_k_to_the_rotation():
     q_rot, k_rot, vp2 = R.rope_kv_append(kp, vp, data.q, data.k_new, data.v_new, data.desc, bt, 16, 1e6)
     assert np.array_equal(vp2, OK.append(kp, vp, data.k_new, data.v_new, data.desc, bt, 16)[1])
     assert q_rot.shape == data.q.shape and k_rot.shape == data.k_new.shape
+
+
+def test_f64_to_bf16_rounding():
+    """Nearest-even on the 8-bit significand grid: exact values stay, halfway cases go to
+    the even neighbour, everything else to the nearer one; the bit patterns decode back."""
+    one_ulp = 2.0 ** -7
+    cases = {1.0: 1.0, 1.0 + one_ulp / 2: 1.0, 1.0 + 3 * one_ulp / 2: 1.0 + 2 * one_ulp,
+             1.0 + one_ulp * 0.51: 1.0 + one_ulp, -3.0: -3.0, 0.0: 0.0,
+             2.0 - one_ulp / 4: 2.0, 255.5: 256.0, 1e-3: None}
+    for x, want in cases.items():
+        got = float(R.bf16_bits_to_f64(R.f64_to_bf16_bits([x]))[0])
+        if want is None:
+            assert abs(got - x) <= 2.0 ** -9 * abs(x)
+        else:
+            assert got == want, (x, got, want)
+    g = np.random.default_rng(6)
+    bits = g.integers(0, 1 << 16, size=4000, dtype=np.uint16)
+    bits = bits[((bits >> 7) & 0xFF) != 0xFF]             # finite patterns only
+    vals = R.bf16_bits_to_f64(bits)
+    fin = np.isfinite(vals) & (np.abs(vals) > 1e-30) & (np.abs(vals) < 1e30)
+    assert np.array_equal(R.f64_to_bf16_bits(vals[fin]), bits[fin])
