@@ -32,7 +32,9 @@ WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              # 36-layer P-PAS serving trace (64 requests)
              "trace": None,
              # one prompt prefilled as several chunks vs as one chunk
-             "chunks": None}
+             "chunks": None,
+             # rotary embedding fused with the page write, on the new rows of a full-size step
+             "rope-mbt2048": ("rope", 2), "rope-mbt16384": ("rope", 3)}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -42,18 +44,18 @@ KERNEL_SOURCES = ["paper_2608_15171_amd/csrc/attn_step.hip", "paper_2608_15171_a
                   "paper_2608_15171_amd/csrc/plan.h"]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the attention kernel from the committed rocprofv3 byte
-    counters (calibrated against a plain copy), or None when no record exists or the
-    kernel sources changed since the counters were taken."""
+def measured_traffic(workload: str, kernel: str = "attn_step_kernel"):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 byte counters
+    (calibrated against a plain copy), or None when no record exists or the kernel
+    sources changed since the counters were taken."""
     import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
-    path = os.path.join(root, "profiles", f"attn_step_kernel.{workload}.traffic.json")
+    path = os.path.join(root, "profiles", f"{kernel}.{workload}.traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     h = hashlib.sha256()
-    for src in KERNEL_SOURCES:
+    for src in rec.get("sources", KERNEL_SOURCES):
         h.update(open(os.path.join(root, src), "rb").read())
     if rec.get("kernel_sources_sha256") != h.hexdigest():
         return None
@@ -185,6 +187,105 @@ def run_trace_workload(args):
     print(json.dumps(rec), flush=True)
 
 
+def run_rope_workload(args, cfg):
+    """ppas_rope_kv_append on the new rows of a full-size step (rotate Q in place, rotated K
+    and plain V into the pages), timed beside ppas_kv_append of the same rows; kernel
+    time from events its launch records. HBM-bound: the algorithmic bytes are Q read and
+    written once plus the new K/V read once and written once."""
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import inputs as I
+    from paper_2608_15171_amd import ppas
+    from paper_2608_15171_amd.hip_events import HipEvents
+    from paper_2608_15171_amd.step import DeviceStep, bits_of
+
+    spec = I.CONFIGS[cfg](args.seed)
+    data = I.make_step_data(spec, args.seed, with_history=False)
+    bt, npages = I.make_block_table(spec, args.seed, permute=True)
+    ds = DeviceStep(data, bt, npages)
+    theta = args.rope_theta
+    # one call on the original rows, kept for the parity sample
+    ds.rope_append(theta)
+    torch.cuda.synchronize()
+    q_rot = bits_of(ds.q)
+    hip = HipEvents()
+    K = args.steps
+
+    def timed(fn):
+        ev = [(hip.create(), hip.create()) for _ in range(K)]
+        for i in range(K):
+            ppas.set_profile_events(*ev[i])
+            fn(i)
+            ppas.set_profile_events(None, None)
+        torch.cuda.synchronize()
+        t = [hip.elapsed_ms(a, b) * 1e3 for a, b in ev]
+        for a, b in ev:
+            hip.destroy(a)
+            hip.destroy(b)
+        return t
+
+    rope = lambda i: ds.rope_append(theta, validate=False)       # noqa: E731  (rotates q again: norms kept)
+    plain = lambda i: ds.append(validate=False)                  # noqa: E731
+    W = warm_up(rope, args)
+    t_rope = timed(rope)
+    warm_up(plain, args)
+    t_plain = timed(plain)
+    us, us_plain = float(np.median(t_rope)), float(np.median(t_plain))
+    T, D = spec.n_rows, spec.head_dim
+    B = float(T * (2 * spec.n_q_heads * D * 2 + 2 * 2 * spec.n_kv_heads * D * 2))
+    B_plain = float(T * 2 * 2 * spec.n_kv_heads * D * 2)
+    gbps = B / (us * 1e-6) / 1e9
+    rec = {
+        "metric": METRIC,
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(us * 1e-3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"rope-append-{spec.name}", "new_rows": T, "rope_theta": theta,
+                   "heads": f"{spec.n_q_heads}q/{spec.n_kv_heads}kv", "head_dim": D, "page_size": 16,
+                   "block_table": "seeded permutation"},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gbps / PEAK_GBPS, 4), "traffic": measured_traffic(
+                         f"rope-mbt{2048 if cfg == 2 else 16384}", kernel="rope_append_kernel"),
+                     "kernel": "rope_append_kernel", "kernel_us": round(us, 2), "kernel_us_min": round(min(t_rope), 2),
+                     "per_launch": {"bytes": B}},
+        "plain_kv_append": {"kernel_us": round(us_plain, 2), "bytes": B_plain,
+                            "gbps": round(B_plain / (us_plain * 1e-6) / 1e9, 2)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle.rope as R
+        rows = np.arange(T)
+        n = min(T, 64)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            sample = rows[(reps * n) % T:(reps * n) % T + n]
+            R.rotate(R.bf16_bits_to_f64(data.q[sample]), R.row_positions(data.desc)[sample], theta)
+            reps += 1
+            if time.perf_counter() - t0 >= min(args.cpu_seconds, 5.0):
+                break
+        dt = time.perf_counter() - t0
+        bytes_cpu = reps * n * spec.n_q_heads * D * 2 * 2
+        rec["cpu_baseline"] = {"value": round(bytes_cpu / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{reps} x {n} query rows rotated by the fp64 NumPy oracle in {dt:.1f} s"}
+        q_ref, _ = R.rope_step(data.q, data.k_new, data.desc, theta)
+        x = R.bf16_bits_to_f64(data.q)
+        pair = np.abs(x[..., :D // 2]) + np.abs(x[..., D // 2:])
+        tol = 2.0 ** -8 * np.abs(q_ref) + 1e-6 * np.concatenate([pair, pair], axis=-1)
+        err = np.abs(R.bf16_bits_to_f64(q_rot) - q_ref)
+        rec["parity"] = {"rows": int(T), "max_abs": float(err.max()), "within_bound": bool((err <= tol).all()),
+                         "bound": "2^-8 |exact| + 1e-6 (|x_i| + |x_(i+64)|) per element"}
+    print(json.dumps(rec), flush=True)
+
+
 def run_chunks_workload(args):
     """One prompt prefilled in chunks of --chunk tokens and as a single chunk: the
     attention time of each schedule (kernel time from HIP events, medians)."""
@@ -265,6 +366,7 @@ def main():
     ap.add_argument("--trace-mbt", type=int, default=16384, help="trace workload: global token budget")
     ap.add_argument("--prompt", type=int, default=16384, help="chunks workload: prompt tokens")
     ap.add_argument("--chunk", type=int, default=2048, help="chunks workload: tokens per chunk")
+    ap.add_argument("--rope-theta", type=float, default=1e6, help="rope workloads: rotary base")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
@@ -285,6 +387,8 @@ def main():
         return run_trace_workload(args)
     if args.workload == "chunks":
         return run_chunks_workload(args)
+    if isinstance(WORKLOADS[args.workload], tuple):
+        return run_rope_workload(args, WORKLOADS[args.workload][1])
     key = WORKLOADS[args.workload]
     spec = (I.CONFIGS[key] if isinstance(key, int) else I.DIAGNOSTICS[key])(args.seed)
     data = I.make_step_data(spec, args.seed)

@@ -114,6 +114,33 @@ ppas_status ppas_kv_append(const ppas_shape* shape, void* k_pages, void* v_pages
                            const int32_t* block_table_host, void* hip_stream);
 
 /*
+ * Rotary position embedding of the step's new rows, fused with the append.
+ * The paper does not describe positional encoding; the operation is the
+ * standard rotary embedding (RoPE) in rotate-half form over the whole head,
+ * applied to the new query and key rows of a decoder block's attention
+ * (Section 6.1) before they are used and cached. For every request s and
+ * i < n_query: row r = query_start + i at position p = cached_len + i; for
+ * every pair j < 64 the angle is a = p * rope_theta^(-2j/128), and a head row x
+ * becomes (x_j cos a - x_{j+64} sin a) at j and (x_{j+64} cos a + x_j sin a) at
+ * j + 64.
+ *   q [T][n_q_heads][128] bf16: every query head row r is rotated in place.
+ *   k_new [T][n_kv_heads][128] bf16: rotated and written to k_pages at (page,
+ *     slot) exactly as ppas_kv_append writes keys; k_new itself is not modified.
+ *   v_new: copied to v_pages unrotated, bit-exact, as ppas_kv_append does.
+ * Angles are reduced in fp64, cos/sin taken in fp32, the rotation computed in
+ * fp32 and rounded to bf16 nearest-even. Nothing else in q or the pools is
+ * written. rope_theta must be finite and > 0 (else PPAS_EINVAL); q must not
+ * be NULL. Validation, ownership and errors otherwise as ppas_kv_append. Call
+ * it in place of ppas_kv_append, before ppas_attn_step, on the same stream.
+ */
+ppas_status ppas_rope_kv_append(const ppas_shape* shape, float rope_theta, void* q,
+                                void* k_pages, void* v_pages,
+                                const void* k_new, const void* v_new,
+                                const ppas_seq* seqs, int32_t n_seqs,
+                                const int32_t* block_table_dev, int32_t bt_stride,
+                                const int32_t* block_table_host, void* hip_stream);
+
+/*
  * Device workspace that ppas_attn_step needs for this step description on the
  * current device: fp32 partial results of rows whose keys are split across
  * workgroups (at least 256 bytes). Depends only on the shape, the descriptors
@@ -182,13 +209,15 @@ ppas_status ppas_set_split_keys(int32_t prefill_split, int32_t decode_split);
 ppas_status ppas_set_tile_positions(int32_t tile_positions);
 
 /*
- * Profiling hook (process-wide). When both are non-NULL, the next
- * ppas_attn_step calls have the packed attention kernel's launch record
- * `start_event` when the kernel starts and `stop_event` when it ends
- * (hipEvent_t handles created by the caller; hipExtLaunchKernel's events), so
- * the kernel's own duration can be read with hipEventElapsedTime. Pass NULLs to
- * stop recording. The events are re-recorded by every call; the caller owns and
- * destroys them.
+ * Profiling hook (process-wide). When both are non-NULL, the following calls
+ * have their kernel launches record `start_event` when the kernel starts and
+ * `stop_event` when it ends (hipEvent_t handles created by the caller;
+ * hipExtLaunchKernel's events), so a kernel's own duration can be read with
+ * hipEventElapsedTime: in ppas_attn_step the packed attention kernel (not the
+ * split merge), in ppas_kv_append and ppas_rope_kv_append their page-write
+ * kernel (start at the first launch, stop at the last when a call needs several
+ * launches for over 64 requests). Pass NULLs to stop recording. The events are
+ * re-recorded by every call; the caller owns and destroys them.
  * Returns PPAS_EINVAL if exactly one of them is NULL.
  */
 ppas_status ppas_set_profile_events(void* start_event, void* stop_event);

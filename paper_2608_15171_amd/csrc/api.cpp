@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -19,7 +20,11 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
                             hipEvent_t ev_start, hipEvent_t ev_stop);
 hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
                             const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
-                            int32_t hkv, hipStream_t stream);
+                            int32_t hkv, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
+hipError_t launch_rope_append(uint16_t* q, uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
+                              const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
+                              int32_t hq, int32_t hkv, double theta, hipStream_t stream, hipEvent_t ev_start,
+                              hipEvent_t ev_stop);
 
 namespace {
 
@@ -221,7 +226,33 @@ ppas_status ppas_kv_append(const ppas_shape* shape, void* k_pages, void* v_pages
     const hipError_t e = launch_kv_append(static_cast<uint16_t*>(k_pages), static_cast<uint16_t*>(v_pages),
                                           static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
                                           seqs, n_seqs, block_table_dev, bt_stride, shape->n_kv_heads,
-                                          static_cast<hipStream_t>(hip_stream));
+                                          static_cast<hipStream_t>(hip_stream),
+                                          static_cast<hipEvent_t>(g_ev_start.load()),
+                                          static_cast<hipEvent_t>(g_ev_stop.load()));
+    return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
+  } catch (...) {
+    return PPAS_EINVAL;
+  }
+}
+
+ppas_status ppas_rope_kv_append(const ppas_shape* shape, float rope_theta, void* q, void* k_pages, void* v_pages,
+                                const void* k_new, const void* v_new, const ppas_seq* seqs, int32_t n_seqs,
+                                const int32_t* block_table_dev, int32_t bt_stride,
+                                const int32_t* block_table_host, void* hip_stream) {
+  try {
+    if (!std::isfinite(rope_theta) || !(rope_theta > 0.f)) return PPAS_EINVAL;
+    ppas_status st = validate(shape, seqs, n_seqs, block_table_host, bt_stride, true);
+    if (st != PPAS_OK) return st;
+    if (n_seqs == 0) return PPAS_OK;
+    if (!q || !k_pages || !v_pages || !k_new || !v_new || !block_table_dev) return PPAS_EINVAL;
+    if (!current_device().gfx950) return PPAS_EUNSUPPORTED;
+    const hipError_t e = launch_rope_append(static_cast<uint16_t*>(q), static_cast<uint16_t*>(k_pages),
+                                            static_cast<uint16_t*>(v_pages), static_cast<const uint16_t*>(k_new),
+                                            static_cast<const uint16_t*>(v_new), seqs, n_seqs, block_table_dev,
+                                            bt_stride, shape->n_q_heads, shape->n_kv_heads, double(rope_theta),
+                                            static_cast<hipStream_t>(hip_stream),
+                                            static_cast<hipEvent_t>(g_ev_start.load()),
+                                            static_cast<hipEvent_t>(g_ev_stop.load()));
     return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
   } catch (...) {
     return PPAS_EINVAL;

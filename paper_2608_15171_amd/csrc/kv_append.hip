@@ -7,6 +7,7 @@
 // of one head is 128 feature rows of 16 tokens: thread t owns the chunk
 // (feature t/2, slots 8(t%2)..+7), gathers those slots from the new rows, and
 // stores the whole chunk when all 8 slots are new, else only the new elements.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
 
 hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
                             const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
-                            int32_t hkv, hipStream_t stream) {
+                            int32_t hkv, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
   for (int32_t s0 = 0; s0 < n_seqs; s0 += kAppendMaxSeqs) {
     AppendArgs a;
     a.kp = kp;
@@ -105,7 +106,10 @@ hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, cons
       blocks += last - first + 1;
     }
     a.blk_start[a.n] = blocks;
-    hipLaunchKernelGGL(kv_append_kernel, dim3(blocks, hkv), dim3(256), 0, stream, a);
+    // profiling events (optional): the first launch records the start, the last one the stop
+    const bool last = s0 + kAppendMaxSeqs >= n_seqs;
+    hipExtLaunchKernelGGL(kv_append_kernel, dim3(blocks, hkv), dim3(256), 0, stream, s0 == 0 ? ev_start : nullptr,
+                          last ? ev_stop : nullptr, 0, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

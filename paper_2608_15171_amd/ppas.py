@@ -64,6 +64,8 @@ _lib.ppas_validate_step.restype = ctypes.c_int
 _lib.ppas_validate_step.argtypes = [_P, _vp, _i32, _vp, _i32]
 _lib.ppas_kv_append.restype = ctypes.c_int
 _lib.ppas_kv_append.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
+_lib.ppas_rope_kv_append.restype = ctypes.c_int
+_lib.ppas_rope_kv_append.argtypes = [_P, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
 _lib.ppas_attn_workspace_bytes.restype = _sz
 _lib.ppas_attn_workspace_bytes.argtypes = [_P, _vp, _i32]
 _lib.ppas_attn_step.restype = ctypes.c_int
@@ -140,6 +142,18 @@ def kv_append(shape: Shape, k_pages, v_pages, k_new, v_new, desc, bt_dev, bt_hos
                              _dev(k_new, "k_new"), _dev(v_new, "v_new"), _host_ptr(d), len(d),
                              _dev(bt_dev, "block_table"), bt_dev.shape[1], _host_ptr(bt), _stream(stream))
     _check(st, "ppas_kv_append")
+
+
+def rope_kv_append(shape: Shape, theta: float, q, k_pages, v_pages, k_new, v_new, desc, bt_dev, bt_host=None,
+                   stream=None) -> None:
+    """Rotate q in place and k_new into the pages at each row's position; copy v_new."""
+    d = _desc(desc)
+    bt = _bt_host(bt_host)
+    st = _lib.ppas_rope_kv_append(ctypes.byref(shape), float(theta), _dev(q, "q"), _dev(k_pages, "k_pages"),
+                                  _dev(v_pages, "v_pages"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
+                                  _host_ptr(d), len(d), _dev(bt_dev, "block_table"), bt_dev.shape[1],
+                                  _host_ptr(bt), _stream(stream))
+    _check(st, "ppas_rope_kv_append")
 
 
 def attn_workspace_bytes(shape: Shape, desc) -> int:

@@ -7,12 +7,13 @@ Inputs (one directory per workload, as written by the commands in the summary):
   <calib>/{FETCH_SIZE,WRITE_SIZE}/run_counter_collection.csv   the same counters for calibrate.py
   <dir>/trace_bench.json                                 bench.py's JSON line of the traced run
 
-Writes profiles/attn_step_kernel.<workload>.md and .traffic.json. The byte
-counters are scaled by what they read for a plain copy of known size; the
-record carries a hash of the kernel and planner sources so bench.py reports
-the traffic only while those sources are unchanged.
+Writes profiles/<kernel>.<workload>.md and .traffic.json. The byte counters
+are scaled by what they read for a plain copy of known size; the record carries
+a hash of the kernel's sources (for the attention kernel, with the planner's) so
+bench.py reports the traffic only while those sources are unchanged.
 
-Usage: python -m paper_2608_15171_amd.profile_summary <workload> <dir> <calib_dir>
+Usage: python -m paper_2608_15171_amd.profile_summary <workload> <dir> <calib_dir> [kernel]
+       (kernel: attn_step_kernel, the default, or rope_append_kernel)
 """
 from __future__ import annotations
 
@@ -23,14 +24,26 @@ import os
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-KERNEL_SOURCES = ["paper_2608_15171_amd/csrc/attn_step.hip", "paper_2608_15171_amd/csrc/plan.cpp",
-                  "paper_2608_15171_amd/csrc/plan.h"]
-KERNEL = "attn_step_kernel"
+SOURCES = {
+    "attn_step_kernel": ["paper_2608_15171_amd/csrc/attn_step.hip", "paper_2608_15171_amd/csrc/plan.cpp",
+                         "paper_2608_15171_amd/csrc/plan.h"],
+    "rope_append_kernel": ["paper_2608_15171_amd/csrc/rope_append.hip"],
+}
+DESCRIPTION = {
+    "attn_step_kernel": "One packed attention launch of the mixed step on one MI355X (gfx950); bf16 inputs, fp32 "
+                        "accumulation.",
+    "rope_append_kernel": "The rotary embedding of a step's new rows fused with their page write, one launch on one "
+                          "MI355X (gfx950); bf16 in and out, fp32 rotation.",
+}
+ALGORITHMIC = {
+    "attn_step_kernel": "algorithmic bytes (visible K/V once + Q + O)",
+    "rope_append_kernel": "algorithmic bytes (Q read and written, new K/V read and written, once each)",
+}
 
 
-def sources_hash() -> str:
+def sources_hash(sources) -> str:
     h = hashlib.sha256()
-    for src in KERNEL_SOURCES:
+    for src in sources:
         h.update(open(os.path.join(ROOT, src), "rb").read())
     return h.hexdigest()
 
@@ -46,14 +59,14 @@ def counter_per_dispatch(path: str, name_part: str, counter: str):
     return sum(per.values()) / len(per), len(per)
 
 
-def main(workload: str, d: str, calib: str):
+def main(workload: str, d: str, calib: str, kernel: str = "attn_step_kernel"):
     stats = list(csv.DictReader(open(os.path.join(d, "trace", "run_kernel_stats.csv"))))
     bench = json.loads(open(os.path.join(d, "trace_bench.json")).read().strip().splitlines()[-1])
     wl_name = bench["config"]["workload"]
-    attn = [r for r in stats if KERNEL in r["Name"]]
+    attn = [r for r in stats if kernel in r["Name"]]
     total = sum(float(r["TotalDurationNs"]) for r in stats)
-    fetch_kib, nf = counter_per_dispatch(os.path.join(d, "FETCH_SIZE", "run_counter_collection.csv"), KERNEL, "FETCH_SIZE")
-    write_kib, nw = counter_per_dispatch(os.path.join(d, "WRITE_SIZE", "run_counter_collection.csv"), KERNEL, "WRITE_SIZE")
+    fetch_kib, nf = counter_per_dispatch(os.path.join(d, "FETCH_SIZE", "run_counter_collection.csv"), kernel, "FETCH_SIZE")
+    write_kib, nw = counter_per_dispatch(os.path.join(d, "WRITE_SIZE", "run_counter_collection.csv"), kernel, "WRITE_SIZE")
     mib = 1024
     copy_bytes = mib * 1024 * 1024
     cf, _ = counter_per_dispatch(os.path.join(calib, "FETCH_SIZE", "run_counter_collection.csv"), "UnaryFunctor", "FETCH_SIZE")
@@ -63,14 +76,15 @@ def main(workload: str, d: str, calib: str):
     fetch_b = fetch_kib * 1024 * ffac
     write_b = write_kib * 1024 * wfac
     alg = bench["roofline"]["per_launch"]["bytes"]
-    rec = {"kernel": KERNEL, "workload": wl_name, "kernel_sources_sha256": sources_hash(), "sources": KERNEL_SOURCES,
+    rec = {"kernel": kernel, "workload": wl_name, "kernel_sources_sha256": sources_hash(SOURCES[kernel]),
+           "sources": SOURCES[kernel],
            "fetch_bytes_per_launch": fetch_b, "write_bytes_per_launch": write_b, "fetch_factor": ffac,
            "write_factor": wfac, "fetch_kib": fetch_kib, "write_kib": write_kib}
-    out = os.path.join(ROOT, "profiles", f"{KERNEL}.{workload}")
+    out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}")
     json.dump(rec, open(out + ".traffic.json", "w"), indent=1)
     cmd = f"bench.py --workload {workload} --no-cpu-baseline"
-    lines = [f"# {KERNEL} -- workload {wl_name} ({workload})", "",
-             "One packed attention launch of the mixed step on one MI355X (gfx950); bf16 inputs, fp32 accumulation.", "",
+    lines = [f"# {kernel} -- workload {wl_name} ({workload})", "",
+             DESCRIPTION[kernel], "",
              "## Kernel trace (rocprofv3 --kernel-trace --stats)", "", "Command:", "",
              f"    cd /tmp && TMPDIR=/tmp rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- "
              f"python3 <repo>/{cmd}", "",
@@ -101,11 +115,11 @@ def main(workload: str, d: str, calib: str):
               f"| WRITE_SIZE (KiB, mean of {nw} launches) | {write_kib:.0f} |",
               f"| bytes read from memory | {fetch_b / 1e6:.1f} MB |",
               f"| bytes written | {write_b / 1e6:.1f} MB |",
-              f"| algorithmic bytes (visible K/V once + Q + O) | {alg / 1e6:.1f} MB |",
+              f"| {ALGORITHMIC[kernel]} | {alg / 1e6:.1f} MB |",
               f"| measured / algorithmic | {(fetch_b + write_b) / alg:.2f} |", ""]
     open(out + ".md", "w").write("\n".join(lines))
     print(out + ".md")
 
 
 if __name__ == "__main__":
-    main(*sys.argv[1:4])
+    main(*sys.argv[1:5])

@@ -67,6 +67,11 @@ class DeviceStep:
         ppas.kv_append(self.shape, self.k_pages, self.v_pages, self.k_new, self.v_new, self.desc, self.bt,
                        self.bt_host if validate else None, stream)
 
+    def rope_append(self, theta: float, stream=None, validate: bool = True) -> None:
+        """Rotate Q in place and the new K into the pages (rotary embedding), copy the new V."""
+        ppas.rope_kv_append(self.shape, theta, self.q, self.k_pages, self.v_pages, self.k_new, self.v_new,
+                            self.desc, self.bt, self.bt_host if validate else None, stream)
+
     def attend(self, stream=None, validate: bool = True) -> None:
         ppas.attn_step(self.shape, self.out, self.q, self.k_pages, self.v_pages, self.desc, self.bt,
                        self.workspace, self.bt_host if validate else None, stream)

@@ -99,6 +99,15 @@ def test_calls_reject_bad_input_before_any_device_work():
     assert st == ppas.PPAS_EINVAL
     assert ppas.attn_workspace_bytes(sh, bad) == 0
     assert ppas.attn_workspace_bytes(sh, GOOD) > 0
+    for theta in (0.0, -1.0, float("nan"), float("inf")):
+        st = ppas._lib.ppas_rope_kv_append(ctypes.byref(sh), theta, 1, 1, 1, 1, 1, GOOD.ctypes.data, 2,
+                                           1, 3, BT.ctypes.data, None)
+        assert st == ppas.PPAS_EINVAL, theta
+    st = ppas._lib.ppas_rope_kv_append(ctypes.byref(sh), 1e6, 1, 1, 1, 1, 1, bad.ctypes.data, 1, 1, 3, None, None)
+    assert st == ppas.PPAS_EINVAL
+    st = ppas._lib.ppas_rope_kv_append(ctypes.byref(sh), 1e6, None, 1, 1, 1, 1, GOOD.ctypes.data, 2, 1, 3,
+                                       BT.ctypes.data, None)
+    assert st == ppas.PPAS_EINVAL                               # no q
 
 
 def check_coverage(spec, items):
