@@ -214,3 +214,30 @@ def test_decode_items_never_exceed_the_page_id_capacity(decode_split):
     assert (dec[:, 7] - dec[:, 6]).max() <= 16384
     assert (dec[:, 6] % 32 == 0).all(), "decode key ranges start on 32-key blocks"
     check_coverage(spec, items)
+
+
+@pytest.mark.parametrize("num_cus", [256, 80])
+def test_decode_only_steps_take_even_pieces_about_one_per_cu(num_cus):
+    """A step of decode rows only: each (row, KV head) stream is cut into even pieces
+    on 32-key blocks, about one item per CU over the step; an explicit decode split
+    keeps the fixed-size pieces."""
+    spec = I.config_pressure_decode_only(0)
+    items = ppas.plan_items(shape(), spec.descriptors(), num_cus=num_cus)
+    assert (items[:, 0] == 1).all()
+    kend = np.array([c + 1 for _, _, c in spec.descriptors().tolist()] * 2)     # one stream per KV head
+    want = np.maximum(-(-kend // (16384 - 32)), (kend * num_cus + kend.sum() // 2) // kend.sum())
+    assert len(items) == want.sum(), (len(items), want.sum())
+    if num_cus == 256:
+        assert 0.8 * num_cus <= len(items) <= 1.25 * num_cus, len(items)
+    assert (items[:, 6] % 32 == 0).all() and (items[:, 7] - items[:, 6]).max() <= 16384
+    for (s, g) in {(int(a), int(b)) for a, b in items[:, 1:3]}:
+        mine = items[(items[:, 1] == s) & (items[:, 2] == g)]
+        span = mine[:, 7] - mine[:, 6]
+        assert span.max() - span.min() < 64, (s, g, span)     # boundaries on 32-key blocks
+    check_coverage(spec, items)
+    ppas.set_split_keys(0, 4096)
+    try:
+        fixed = ppas.plan_items(shape(), spec.descriptors(), num_cus=num_cus)
+    finally:
+        ppas.set_split_keys(0, 0)
+    assert ((fixed[:, 7] - fixed[:, 6]) <= 4096).all() and (fixed[:, 6] % 4096 == 0).all()

@@ -307,6 +307,22 @@ def test_long_contexts_sampled(lib, decode_split):
     compare(out, ref, rows=rows, label=f"long contexts sampled {len(rows)} rows")
 
 
+@pytest.mark.parametrize("case", ["pressure-decode", "long", "tiny"])
+def test_decode_only_steps(lib, case):
+    """Steps of decode rows only take even key pieces, about one item per CU: the 48
+    rows of the pressure step, long contexts (several pieces forced by the per-item
+    key capacity), and many rows with a few keys (pieces collapse to one)."""
+    if case == "pressure-decode":
+        spec = I.config_pressure_decode_only(0)
+    elif case == "long":
+        spec = I.StepSpec("long-decodes", [I.Seq(1, c, i) for i, c in enumerate([131071, 65536, 40000, 17, 0])])
+    else:
+        spec = I.StepSpec("tiny-decodes", [I.Seq(1, c, i) for i, c in enumerate(range(0, 300, 7))])
+    print(f"decode-only {case}: rows={spec.n_rows}", flush=True)
+    data, ds = run_step(lib, spec, 3)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"decode-only {case}")
+
+
 def test_steps_on_two_streams(lib):
     """Two different steps submitted alternately on two streams, each with its own workspace,
     enough times to wrap the library's staging ring; both match the oracle."""
