@@ -262,7 +262,11 @@ __device__ __forceinline__ void prefill_tile(const StepArgs& a, const WorkItem& 
   PrefillCtx c;
   c.a = &a;
   c.lane = tid & 63;
-  c.w = tid >> 6;
+  // In the eight-wave shape the wave index is declared wave-uniform, so the page
+  // selects and page bases of the LDS transfers stay on the scalar unit (16 % fewer
+  // vector instructions in the main loop, ~1 % faster); the four-wave shape measured
+  // ~1 % slower that way and keeps the per-lane form.
+  c.w = kW == 8 ? int(__builtin_amdgcn_readfirstlane(tid >> 6)) : tid >> 6;
   c.n = c.lane & 31;
   c.h = c.lane >> 5;
   {
