@@ -8,7 +8,9 @@
  * an iteration). Prefill and decode store each token's key and value in the KV
  * cache (Section 2), which is paged (Section 7, PagedAttention). A step is two
  * calls on one stream: ppas_kv_append writes the step's new keys/values into
- * the pages, then ppas_attn_step computes the attention of every query row.
+ * the pages (or ppas_rope_kv_append, which first rotates the new query and key
+ * rows by their positions), then ppas_attn_step computes the attention of
+ * every query row.
  *
  * Conventions shared by every entry point
  *   - bf16 means IEEE bfloat16 bit patterns (uint16 in memory).
