@@ -673,6 +673,7 @@ __global__ __launch_bounds__(threads_of<kW>(), kW == 4 ? 2 : 1) void attn_step_k
 // Block (item, y) handles rows 8y..8y+7 of the item; 32 lanes per row, 4
 // features per lane.
 constexpr int kCombineRowsPerBlock = 8;
+constexpr int kMergeBatch = 4;            // splits whose loads a merge thread issues together
 constexpr int kCombineThreads = 32 * kCombineRowsPerBlock;
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineItem* items, const float2* part_ml,
                                                            const float* part_acc, uint16_t* out, int hq) {
@@ -681,18 +682,36 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineI
   const int r = blockIdx.y * kCombineRowsPerBlock + (threadIdx.x >> 5);
   if (r >= rows) return;
   const int d0 = (threadIdx.x & 31) * 4;
-  float M = kNegInf;
-  for (int s = 0; s < ci.nsplit; ++s) M = fmaxf(M, part_ml[ci.part + s * rows + r].x);
-  const float M_use = (M == kNegInf) ? 0.f : M;
-  float L = 0.f;
+  // Splits are merged in batches of kMergeBatch whose (m, l) and accumulator loads
+  // are all issued before any is used (one memory round trip per batch); a later
+  // batch rescales what is merged so far to its larger maximum. Absent splits of a
+  // batch enter with m = -inf and weigh 0. Every split gives each of its rows at
+  // least one key, so a real split's m is finite.
+  float M = kNegInf, L = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int s = 0; s < ci.nsplit; ++s) {
-    const int slot = ci.part + s * rows + r;
-    const float2 ml = part_ml[slot];
-    const float f = fast_exp2(ml.x - M_use);
-    L += f * ml.y;
-    acc += f * *reinterpret_cast<const f32x4*>(part_acc + size_t(slot) * kHeadDim + d0);
+  for (int s0 = 0; s0 < ci.nsplit; s0 += kMergeBatch) {
+    float2 ml[kMergeBatch];
+    f32x4 pa[kMergeBatch];
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const int slot = ci.part + min(s0 + i, ci.nsplit - 1) * rows + r;
+      ml[i] = part_ml[slot];
+      pa[i] = *reinterpret_cast<const f32x4*>(part_acc + size_t(slot) * kHeadDim + d0);
+      if (s0 + i >= ci.nsplit) ml[i].x = kNegInf;
+    }
+    float Mb = M;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) Mb = fmaxf(Mb, ml[i].x);
+    const float sc = fast_exp2(M - Mb);      // 0 while nothing is merged (M = -inf)
+    L *= sc;
+    acc *= sc;
+#pragma unroll
+    for (int i = 0; i < kMergeBatch; ++i) {
+      const float f = fast_exp2(ml[i].x - Mb);
+      L += f * ml[i].y;
+      acc += f * pa[i];
+    }
+    M = Mb;
   }
   const float inv = 1.f / L;
   uint16_t* orow = out + (size_t(ci.row0 + r / kGroup) * hq + ci.kvh * kGroup + r % kGroup) * kHeadDim + d0;
