@@ -404,15 +404,15 @@ def main():
     hip = HipEvents()
     K, W = args.steps, args.warmup
     ev = [(hip.create(), hip.create()) for _ in range(K)]
-    ka = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    ea = [(hip.create(), hip.create()) for _ in range(K)]
 
+    # In the timed steps only the attention kernel's launch records events (its
+    # duration feeds the roofline); the append is timed in a pass of its own after
+    # them, because every extra event in the queue also adds to the step's wall time.
     def one_step(i, timed):
         ds.k_pages, ds.v_pages = pools[i % copies]
-        if timed:
-            ka[i][0].record()
         ds.append()
         if timed:
-            ka[i][1].record()
             ppas.set_profile_events(*ev[i])
         ds.attend()
         if timed:
@@ -424,11 +424,18 @@ def main():
         one_step(i, True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    for i in range(K):
+        ds.k_pages, ds.v_pages = pools[i % copies]
+        ppas.set_profile_events(*ea[i])
+        ds.append()
+        ppas.set_profile_events(None, None)
+        ds.attend()
+    torch.cuda.synchronize()
 
     ms_step = (t1 - t0) / K * 1e3
     attn_ms = [hip.elapsed_ms(a, b) for a, b in ev]
-    app_ms = [a.elapsed_time(b) for a, b in ka]
-    for a, b in ev:
+    app_ms = [hip.elapsed_ms(a, b) for a, b in ea]
+    for a, b in ev + ea:
         hip.destroy(a)
         hip.destroy(b)
     k_ms = float(np.mean(attn_ms))
