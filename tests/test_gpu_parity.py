@@ -235,6 +235,17 @@ def test_attention_full_size_sampled(lib, cfg, tile):
     assert np.isfinite(out).all()
 
 
+@pytest.mark.parametrize("name", ["mbt2048-tp2shard", "pressure-tp2shard"])
+def test_tp2_shard_full_size_sampled(lib, name):
+    """One GPU's half of the MBT=2048 and pressure steps split two ways by KV head
+    (8 query heads, 1 KV head), at full size, on sampled rows."""
+    spec = I.DIAGNOSTICS[name](0)
+    print(f"{name}: rows={spec.n_rows} heads={spec.n_q_heads}/{spec.n_kv_heads}", flush=True)
+    data, ds = run_step(lib, spec, 0, spare=0)
+    rows = sample_rows(spec, I.rng(0, 78))
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows, label=f"{name} sampled")
+
+
 # ------------------------------------------------------------------ serving trace
 
 def test_trace_steps_match_oracle(lib):
