@@ -334,6 +334,42 @@ def test_decode_only_steps(lib, case):
     compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"decode-only {case}")
 
 
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_split_merge_repeated_on_one_workspace(lib, cfg):
+    """Two steps of the same shape with different inputs share one workspace (the split
+    partials) and alternate; every output must equal its own input set's first output
+    bit for bit (a merge that read partials left by the other step's previous call
+    would not), and the outputs match the oracle."""
+    ppas, step, torch = lib
+    spec = I.CONFIGS[cfg](0)
+    runs = []
+    for seed in (0, 1):
+        data = I.make_step_data(spec, seed)
+        bt, npages = I.make_block_table(spec, seed, permute=True)
+        ds = step.DeviceStep(data, bt, npages)
+        ds.fill_history()
+        ds.append()
+        runs.append((data, ds))
+    runs[1][1].workspace = runs[0][1].workspace
+    items = ppas.plan_items(runs[0][1].shape, runs[0][1].desc)
+    print(f"config {cfg}: {len(items)} items, {int((items[:, 6] > 0).sum())} not starting at key 0", flush=True)
+    first = []
+    for rep in range(24):
+        for k, (data, ds) in enumerate(runs):
+            ds.attend()
+            torch.cuda.synchronize()
+            out = step.bits_of(ds.out)
+            if rep == 0:
+                first.append(out)
+            else:
+                assert np.array_equal(out, first[k]), f"repeat {rep}, input set {k}: output changed"
+    g = I.rng(0, 79)
+    for k, (data, ds) in enumerate(runs):
+        rows = sample_rows(spec, g, per_seq=4)
+        compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows,
+                label=f"config{cfg} input set {k} after repeats")
+
+
 def test_steps_on_two_streams(lib):
     """Two different steps submitted alternately on two streams, each with its own workspace,
     enough times to wrap the library's staging ring; both match the oracle."""
