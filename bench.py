@@ -34,7 +34,10 @@ WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              # one prompt prefilled as several chunks vs as one chunk
              "chunks": None,
              # rotary embedding fused with the page write, on the new rows of a full-size step
-             "rope-mbt2048": ("rope", 2), "rope-mbt16384": ("rope", 3)}
+             "rope-mbt2048": ("rope", 2), "rope-mbt16384": ("rope", 3),
+             # the trace under P-PAS and under fixed 16k / 2k budgets: request latencies from
+             # the measured attention time of every iteration
+             "trace-latency": None}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -286,6 +289,54 @@ def run_rope_workload(args, cfg):
     print(json.dumps(rec), flush=True)
 
 
+def run_trace_latency_workload(args):
+    """The 36-layer trace under three budget rules (P-PAS: 16,384 / 2,048 by prefill
+    pressure; fixed 16,384; fixed 2,048), each run on the GPU. From the measured
+    attention + page-write time of every iteration (summed over the layers): the
+    total, and per request the time to first token and time per output token in an
+    iterations-back-to-back time model (attention-only: no other decoder-block work)."""
+    from paper_2608_15171_amd import latency as LT
+    from paper_2608_15171_amd import trace_run as TR
+
+    rules = [("ppas", 16384), ("fixed", 16384), ("fixed", 2048)]
+    per_rule, flops_ppas, t_ppas = {}, None, None
+    banks = None
+    for mode, mbt in rules:
+        setup = TR.make_setup(args.seed, mode=mode, mbt=mbt, layers=args.layers)
+        if banks is None or banks[0].shape[0] < setup.bank_rows:
+            banks = TR.make_banks(args.seed, setup.bank_rows)
+        name = "ppas" if mode == "ppas" else f"fixed{mbt}"
+        print(f"trace-latency: {name}: {len(setup.steps)} steps x {args.layers} layers", file=sys.stderr, flush=True)
+        res = TR.run(setup, banks, args.layers)
+        lat = LT.summarize(LT.request_latencies(setup.requests, setup.steps, res["step_ms"]))
+        per_rule[name] = {"scheduler_steps": len(setup.steps), "attention_ms_total": round(res["attn_ms_total"], 2),
+                          "kv_append_ms_total": round(res["kv_append_ms_total"], 2),
+                          "attention_tflops": round(res["flops"] / (res["attn_ms_total"] * 1e-3) / 1e12, 2), **lat}
+        if mode == "ppas":
+            flops_ppas, t_ppas = res["flops"], res["attn_ms_total"]
+    achieved = flops_ppas / (t_ppas * 1e-3) / 1e12
+    rec = {
+        "metric": METRIC,
+        "value": round(achieved, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": per_rule["ppas"]["scheduler_steps"],
+        "warmup": 0,
+        "ms_per_step": round(t_ppas / per_rule["ppas"]["scheduler_steps"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"trace-latency-64req-{args.layers}layers", "layers": args.layers,
+                   "budget_rules": [n for n in per_rule], "heads": "16q/2kv", "head_dim": 128, "page_size": 16},
+        "latency_attention_only": per_rule,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_TFLOPS, 4), "traffic": None, "kernel": "attn_step_kernel"},
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def run_chunks_workload(args):
     """One prompt prefilled in chunks of --chunk tokens and as a single chunk: the
     attention time of each schedule (kernel time from HIP events, medians)."""
@@ -387,6 +438,8 @@ def main():
         return run_trace_workload(args)
     if args.workload == "chunks":
         return run_chunks_workload(args)
+    if args.workload == "trace-latency":
+        return run_trace_latency_workload(args)
     if isinstance(WORKLOADS[args.workload], tuple):
         return run_rope_workload(args, WORKLOADS[args.workload][1])
     key = WORKLOADS[args.workload]

@@ -151,7 +151,10 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
         ev.destroy(b)
     flops = sum(M.flops(s.spec) for s in setup.steps) * layers
     dec_bytes = sum(M.kv_bytes(s.spec, "decode") for s in setup.steps) * layers
+    # per scheduler iteration: attention + page writes summed over the layers
+    step_ms = (np.asarray(attn_ms) + np.asarray(app_ms)).reshape(len(setup.steps), layers).sum(axis=1)
     return {"attn_ms_total": float(np.sum(attn_ms)), "kv_append_ms_total": float(np.sum(app_ms)),
+            "step_ms": step_ms,
             "wall_ms": t0.elapsed_time(t1), "launches": len(attn_ms), "flops": flops,
             "decode_kv_bytes": dec_bytes, "attn_ms_max": float(np.max(attn_ms)), "checks": checks}
 
