@@ -116,6 +116,41 @@ def _dev(t, name):
     return t.data_ptr()
 
 
+def _rows(d) -> int:
+    return int(d[:, 1].astype(np.int64).clip(min=0).sum()) if len(d) else 0
+
+
+def _need(t, name, nbytes: int, elem: int | None = 2):
+    """Refuse a device buffer smaller than the call will touch (or of the wrong
+    element size), so a bad argument raises here instead of reaching a kernel."""
+    if t is None:
+        return
+    if elem is not None and t.element_size() != elem:
+        raise ValueError(f"{name} must have {elem}-byte elements (bf16 bit patterns), got {t.dtype}")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name} holds {have} bytes; this call needs {nbytes}")
+
+
+def _check_buffers(shape: Shape, d, q=None, out=None, k_new=None, v_new=None, k_pages=None, v_pages=None,
+                   bt_dev=None):
+    if len(d) == 0:
+        return                      # an empty step touches no buffer
+    T, D = _rows(d), shape.head_dim
+    _need(q, "q", T * shape.n_q_heads * D * 2)
+    _need(out, "out", T * shape.n_q_heads * D * 2)
+    _need(k_new, "k_new", T * shape.n_kv_heads * D * 2)
+    _need(v_new, "v_new", T * shape.n_kv_heads * D * 2)
+    pool = int(shape.num_pages) * shape.n_kv_heads * shape.page_size * D * 2
+    _need(k_pages, "k_pages", pool)
+    _need(v_pages, "v_pages", pool)
+    if bt_dev is not None:
+        if bt_dev.element_size() != 4 or bt_dev.dim() != 2:
+            raise ValueError("block_table must be an int32 [n_seqs, stride] device tensor")
+        if bt_dev.shape[0] < len(d):
+            raise ValueError(f"block_table has {bt_dev.shape[0]} rows for {len(d)} requests")
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -138,6 +173,7 @@ def validate_step(shape: Shape, desc, bt_host=None, bt_stride: int | None = None
 def kv_append(shape: Shape, k_pages, v_pages, k_new, v_new, desc, bt_dev, bt_host=None, stream=None) -> None:
     d = _desc(desc)
     bt = _bt_host(bt_host)
+    _check_buffers(shape, d, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_kv_append(ctypes.byref(shape), _dev(k_pages, "k_pages"), _dev(v_pages, "v_pages"),
                              _dev(k_new, "k_new"), _dev(v_new, "v_new"), _host_ptr(d), len(d),
                              _dev(bt_dev, "block_table"), bt_dev.shape[1], _host_ptr(bt), _stream(stream))
@@ -149,6 +185,7 @@ def rope_kv_append(shape: Shape, theta: float, q, k_pages, v_pages, k_new, v_new
     """Rotate q in place and k_new into the pages at each row's position; copy v_new."""
     d = _desc(desc)
     bt = _bt_host(bt_host)
+    _check_buffers(shape, d, q=q, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_rope_kv_append(ctypes.byref(shape), float(theta), _dev(q, "q"), _dev(k_pages, "k_pages"),
                                   _dev(v_pages, "v_pages"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
                                   _host_ptr(d), len(d), _dev(bt_dev, "block_table"), bt_dev.shape[1],
@@ -164,6 +201,7 @@ def attn_workspace_bytes(shape: Shape, desc) -> int:
 def attn_step(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, workspace, bt_host=None, stream=None) -> None:
     d = _desc(desc)
     bt = _bt_host(bt_host)
+    _check_buffers(shape, d, q=q, out=out, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_attn_step(ctypes.byref(shape), _dev(out, "out"), _dev(q, "q"), _dev(k_pages, "k_pages"),
                              _dev(v_pages, "v_pages"), _host_ptr(d), len(d), _dev(bt_dev, "block_table"),
                              bt_dev.shape[1], _host_ptr(bt), _dev(workspace, "workspace"),

@@ -370,6 +370,36 @@ def test_split_merge_repeated_on_one_workspace(lib, cfg):
                 label=f"config{cfg} input set {k} after repeats")
 
 
+def test_binding_refuses_short_buffers(lib):
+    """Buffers smaller than the step needs (or of the wrong element size) raise in the
+    binding before any launch; the pools and outputs are left untouched."""
+    ppas, step, torch = lib
+    spec = I.random_small_step(4, max_seqs=3, max_n=20, max_c=40)
+    data = I.make_step_data(spec, 4)
+    bt, npages = I.make_block_table(spec, 4, spare_pages=2)
+    ds = step.DeviceStep(data, bt, npages, pool_fill=SENTINEL)
+    k0 = step.bits_of(ds.k_pages)
+    short = lambda t: t.reshape(-1)[: t.numel() - 1]          # noqa: E731
+    cases = [
+        lambda: ppas.attn_step(ds.shape, short(ds.out), ds.q, ds.k_pages, ds.v_pages, ds.desc, ds.bt, ds.workspace),
+        lambda: ppas.attn_step(ds.shape, ds.out, short(ds.q), ds.k_pages, ds.v_pages, ds.desc, ds.bt, ds.workspace),
+        lambda: ppas.attn_step(ds.shape, ds.out, ds.q, short(ds.k_pages), ds.v_pages, ds.desc, ds.bt, ds.workspace),
+        lambda: ppas.kv_append(ds.shape, ds.k_pages, ds.v_pages, short(ds.k_new), ds.v_new, ds.desc, ds.bt),
+        lambda: ppas.kv_append(ds.shape, ds.k_pages, short(ds.v_pages), ds.k_new, ds.v_new, ds.desc, ds.bt),
+        lambda: ppas.kv_append(ds.shape, ds.k_pages, ds.v_pages, ds.k_new, ds.v_new, ds.desc, ds.bt[:1]),
+        lambda: ppas.kv_append(ds.shape, ds.k_pages, ds.v_pages, ds.k_new.float(), ds.v_new, ds.desc, ds.bt),
+        lambda: ppas.rope_kv_append(ds.shape, 1e6, short(ds.q), ds.k_pages, ds.v_pages, ds.k_new, ds.v_new,
+                                    ds.desc, ds.bt),
+    ]
+    for k, call in enumerate(cases):
+        if k == 5 and len(ds.desc) < 2:
+            continue
+        with pytest.raises(ValueError):
+            call()
+    torch.cuda.synchronize()
+    assert np.array_equal(step.bits_of(ds.k_pages), k0)
+
+
 def test_steps_on_two_streams(lib):
     """Two different steps submitted alternately on two streams, each with its own workspace,
     enough times to wrap the library's staging ring; both match the oracle."""
