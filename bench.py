@@ -421,7 +421,8 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
-              "multi-GPU mode; see the sharding notes in DESIGN.md", file=sys.stderr)
+              "multi-GPU mode (a step shards by request or by KV head with no exchange, which is not built)",
+              file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
