@@ -117,6 +117,19 @@ def test_attention_fuzz(lib, seed, splits, tile):
     compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"fuzz{seed}/{splits}/tile{tile}")
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_attention_random_plans(lib, seed):
+    """Random mixed steps under random plan choices: tile shape, prefill and decode
+    split sizes (forced small or left to the planner), contexts up to 2,000 keys."""
+    g = np.random.default_rng(9000 + seed)
+    spec = I.random_small_step(7000 + seed, max_seqs=int(g.integers(1, 9)), max_n=int(g.integers(1, 200)),
+                               max_c=int(g.integers(0, 2000)))
+    tile = int(g.choice([0, 16, 32]))
+    splits = (int(g.choice([0, 64, 128, 256, 1024])), int(g.choice([0, 32, 96, 512])))
+    data, ds = run_step(lib, spec, seed, splits=splits, spare=int(g.integers(0, 5)), tile=tile)
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"random plan {seed} tile={tile} splits={splits}")
+
+
 def test_attention_small_config(lib):
     spec = I.config_small(0)
     data, ds = run_step(lib, spec, 0)
