@@ -14,6 +14,8 @@ bench.py reports the traffic only while those sources are unchanged.
 
 Usage: python -m paper_2608_15171_amd.profile_summary <workload> <dir> <calib_dir> [kernel]
        (kernel: attn_step_kernel, the default, or rope_append_kernel)
+       python -m paper_2608_15171_amd.profile_summary --mfma <workload> <dir>
+       (matrix-core utilisation from one counter pass: profiles/attn_step_kernel.<workload>.mfma.md)
 """
 from __future__ import annotations
 
@@ -121,5 +123,54 @@ def main(workload: str, d: str, calib: str, kernel: str = "attn_step_kernel"):
     print(out + ".md")
 
 
+MFMA_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_MFMA",
+                 "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT"]
+
+
+def mfma_summary(workload: str, d: str, kernel: str = "attn_step_kernel", simds: int = 1024, xcds: int = 8):
+    """Matrix-core utilisation of the kernel from one rocprofv3 --pmc pass of MFMA_COUNTERS
+    (<d>/MFMA/run_counter_collection.csv, <d>/MFMA_bench.json). SQ counters are summed over
+    the chip, GRBM_GUI_ACTIVE over the XCDs; means over the pass's last two dispatches."""
+    rows = list(csv.DictReader(open(os.path.join(d, "MFMA", "run_counter_collection.csv"))))
+    per, dur = {}, {}
+    for r in rows:
+        if kernel not in r["Kernel_Name"]:
+            continue
+        c = per.setdefault(r["Dispatch_Id"], {})
+        c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        dur[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    ids = sorted(per, key=int)[-2:]
+    m = {k: sum(per[i][k] for i in ids) / len(ids) for k in MFMA_COUNTERS}
+    us = sum(dur[i] for i in ids) / len(ids)
+    bench = json.loads(open(os.path.join(d, "MFMA_bench.json")).read().strip().splitlines()[-1])
+    flop = bench["roofline"]["per_launch"]["flop"]
+    cycles = m["GRBM_GUI_ACTIVE"] / xcds
+    clock = cycles / us / 1e3
+    busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (simds * cycles)
+    mfma_flop = m["SQ_INSTS_MFMA"] * 32768       # the 32x32x16 bf16 and 16x16x32 bf16 MFMAs both do 2*16384 FLOP
+    cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d <out> -o run "
+           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+    lines = [f"# {kernel} -- matrix-core utilisation, workload {bench['config']['workload']} ({workload})", "",
+             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             "| quantity | value | how it is read |", "|---|---|---|",
+             f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
+             f"| engine clock | {clock:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",
+             f"| MFMA pipe busy | {100 * busy:.1f} % of SIMD cycles | SQ_VALU_MFMA_BUSY_CYCLES / ({simds} SIMDs x cycles) |",
+             f"| MFMA instructions x 32,768 FLOP | {mfma_flop / 1e9:.1f} GFLOP | SQ_INSTS_MFMA; algorithmic FLOP {flop / 1e9:.1f} G "
+             f"(masked keys of diagonal blocks and padded decode heads are executed too) |",
+             f"| MFMA rate at the run's clock | {mfma_flop / (us * 1e-6) / 1e12:.0f} TFLOP/s | executed MFMA FLOP / kernel time |",
+             f"| algorithmic rate | {flop / (us * 1e-6) / 1e12:.0f} TFLOP/s = {100 * flop / (us * 1e-6) / 2.5e15:.1f} % of the 2.5 PFLOP/s bf16 peak | |",
+             f"| VALU instructions per MFMA | {m['SQ_INSTS_VALU'] / m['SQ_INSTS_MFMA']:.2f} | SQ_INSTS_VALU / SQ_INSTS_MFMA (MFMAs included) |",
+             f"| LDS instructions per MFMA | {m['SQ_INSTS_LDS'] / m['SQ_INSTS_MFMA']:.2f} | SQ_INSTS_LDS / SQ_INSTS_MFMA |",
+             f"| LDS busy | {100 * m['SQ_LDS_IDX_ACTIVE'] / (cycles * simds / 4):.1f} % of CU cycles | SQ_LDS_IDX_ACTIVE / (CUs x cycles) |",
+             f"| LDS bank conflict cycles | {m['SQ_LDS_BANK_CONFLICT']:.0f} | SQ_LDS_BANK_CONFLICT |", ""]
+    out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}.mfma.md")
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
 if __name__ == "__main__":
-    main(*sys.argv[1:5])
+    if sys.argv[1] == "--mfma":
+        mfma_summary(*sys.argv[2:4])
+    else:
+        main(*sys.argv[1:5])
