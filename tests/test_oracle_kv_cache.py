@@ -72,3 +72,62 @@ def test_only_written_slots_change_and_round_trip():
         k, v = OK.gather(ka, va, bt[s], c + n, 16)
         assert np.array_equal(k[:c], data.k_hist[s]) and np.array_equal(k[c:], data.k_new[qs:qs + n])
         assert np.array_equal(v[:c], data.v_hist[s]) and np.array_equal(v[c:], data.v_new[qs:qs + n])
+
+
+# ---------------------------------------------------------------- mutation test
+# Plausible mistakes planted in a copy of the oracle's append; the pins above, run
+# against the copy, must reject each one.
+
+MUTANTS = {
+    "slot_off_by_one": ("slot = pos % page_size\n        H, D = k_new", "slot = (pos + 1) % page_size\n        H, D = k_new"),
+    "positions_from_zero": ("pos = c + np.arange(n)", "pos = np.arange(n)"),
+    "logical_page_as_physical": ("page = np.asarray(block_table)[s, pos // page_size]\n        slot = pos % page_size\n        H, D",
+                                 "page = pos // page_size\n        slot = pos % page_size\n        H, D"),
+    "key_features_strided": ("k_new[qs:qs + n].reshape(n, H, D // 8, 8)",
+                             "k_new[qs:qs + n].reshape(n, H, 8, D // 8).transpose(0, 1, 3, 2)"),
+    "rows_from_zero": ("kp[page, :, :, slot, :] = k_new[qs:qs + n]", "kp[page, :, :, slot, :] = k_new[0:n]"),
+    "values_from_keys": ("vp[page, :, :, slot] = v_new[qs:qs + n]", "vp[page, :, :, slot] = k_new[qs:qs + n]"),
+}
+
+
+def mutant(name):
+    import types
+    src = open(OK.__file__).read()
+    a, b = MUTANTS[name]
+    assert src.count(a) == 1, name
+    mod = types.ModuleType("kv_cache_mutant_" + name)
+    exec(compile(src.replace(a, b), "<mutant>", "exec"), mod.__dict__)
+    return mod
+
+
+def pins_pass(mod) -> bool:
+    """The scalar-loop pin (two key chunks per head, several requests per step) and
+    the hand-worked addresses, run against a candidate oracle module."""
+    try:
+        for seed in range(3):
+            spec = I.random_small_step(seed, max_seqs=4, max_n=20, max_c=40)
+            spec.head_dim = 16
+            data = I.make_step_data(spec, seed, with_history=False)
+            bt, npages = I.make_block_table(spec, seed, permute=True, spare_pages=3)
+            kp, vp = pools(npages, 2, 16, 16)
+            a = mod.append(kp, vp, data.k_new, data.v_new, data.desc, bt, 16)
+            b = scalar_append(kp, vp, data.k_new, data.v_new, data.desc, bt, 16)
+            if not (np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])):
+                return False
+        kp, vp = pools(8, 1, 16, 16)
+        k_new = np.arange(48, dtype=np.uint16).reshape(3, 1, 16)
+        ka, va = mod.append(kp, vp, k_new, k_new + 100, np.array([[0, 3, 14]]), np.array([[7, 2]]), 16)
+        if ka[2, 0, 1, 0].tolist() != list(range(40, 48)) or va[7, 0, :, 15].tolist() != list(range(116, 132)):
+            return False
+    except Exception:
+        return False
+    return True
+
+
+def test_pins_accept_the_oracle():
+    assert pins_pass(OK)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_planted_mistake(name):
+    assert not pins_pass(mutant(name)), f"mutant {name} survived the pins"

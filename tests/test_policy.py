@@ -101,3 +101,40 @@ def test_pressure_caps_prefill():
     st = next(s for s in steps if s.index == 2)
     assert st.n_prefill == 2 and st.n_decode == 1 and st.prefill_budget == 2048
     assert [(s.req_id, s.n_query) for s in st.spec.seqs] == [(0, 1), (1, 2048)]
+
+
+# ---------------------------------------------------------------- mutation test
+# Plausible misreadings of Algorithm 1 planted in a copy of the oracle; the printed
+# truth table must reject each one.
+
+MUTANTS = {
+    "strict_threshold": ("if n_p >= n_th and n_d > 0:", "if n_p > n_th and n_d > 0:"),
+    "waiting_prefills_ignored": ("n_p = n_prefill_running + n_prefill_waiting", "n_p = n_prefill_running"),
+    "decodes_ignored": ("if n_p >= n_th and n_d > 0:", "if n_p >= n_th:"),
+    "either_condition": ("if n_p >= n_th and n_d > 0:", "if n_p >= n_th or n_d > 0:"),
+    "budgets_swapped": ("        return b_cap\n    return b_max", "        return b_max\n    return b_cap"),
+}
+
+
+def policy_mutant(name):
+    import types
+    src = open(OP.__file__).read()
+    a, b = MUTANTS[name]
+    assert src.count(a) == 1, name
+    mod = types.ModuleType("policy_mutant_" + name)
+    exec(compile(src.replace(a, b), "<mutant>", "exec"), mod.__dict__)
+    return mod
+
+
+def table_passes(mod) -> bool:
+    return all(mod.prefill_budget(r["prefill_running"], r["prefill_waiting"], r["decode_running"]) == r["B_prefill"]
+               for r in GOLD["truth_table"])
+
+
+def test_truth_table_accepts_the_oracle():
+    assert table_passes(OP)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_truth_table_rejects_planted_mistake(name):
+    assert not table_passes(policy_mutant(name)), f"mutant {name} survived the truth table"
