@@ -298,6 +298,8 @@ ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q, co
     // after a failed launch: a kernel that did start may still read it)
     const bool recorded = hipEventRecord(slot->done, stream) == hipSuccess;
     slot->pending = recorded;
+    // without the event, drain the stream before the slot can be refilled
+    if (!recorded) (void)hipStreamSynchronize(stream);
     return (e == hipSuccess && recorded) ? PPAS_OK : PPAS_EHIP;
   } catch (...) {
     return PPAS_EINVAL;
