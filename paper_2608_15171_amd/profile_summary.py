@@ -169,8 +169,53 @@ def mfma_summary(workload: str, d: str, kernel: str = "attn_step_kernel", simds:
     print(out)
 
 
+STALL_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+                  "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VALU"]
+
+
+def stall_summary(workload: str, d: str, kernel: str = "attn_step_kernel", cus: int = 256, xcds: int = 8):
+    """Where the kernel's waves spend their time, from one rocprofv3 --pmc pass of
+    STALL_COUNTERS (<d>/STALL/run_counter_collection.csv, <d>/STALL_bench.json). The SQ
+    wave counters are wave-cycles in units of 4 cycles, summed over the chip; means over
+    the pass's last two dispatches."""
+    rows = list(csv.DictReader(open(os.path.join(d, "STALL", "run_counter_collection.csv"))))
+    per, dur = {}, {}
+    for r in rows:
+        if kernel not in r["Kernel_Name"]:
+            continue
+        c = per.setdefault(r["Dispatch_Id"], {})
+        c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        dur[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    ids = sorted(per, key=int)[-2:]
+    m = {k: sum(per[i][k] for i in ids) / len(ids) for k in STALL_COUNTERS}
+    us = sum(dur[i] for i in ids) / len(ids)
+    bench = json.loads(open(os.path.join(d, "STALL_bench.json")).read().strip().splitlines()[-1])
+    cycles = m["GRBM_GUI_ACTIVE"] / xcds
+    wave = m["SQ_WAVE_CYCLES"]
+    cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(STALL_COUNTERS)} --output-format csv -d <out> -o run "
+           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+    share = lambda k: f"{100 * m[k] / wave:.1f} % of wave time"
+    lines = [f"# {kernel} -- where the waves spend their time, workload {bench['config']['workload']} ({workload})", "",
+             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             "| quantity | value | how it is read |", "|---|---|---|",
+             f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
+             f"| engine clock | {cycles / us / 1e3:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",
+             f"| resident waves per CU | {4 * wave / (cycles * cus):.2f} | 4 x SQ_WAVE_CYCLES / (CUs x cycles) |",
+             f"| issuing or executing | {share('SQ_ACTIVE_INST_ANY')} | SQ_ACTIVE_INST_ANY / SQ_WAVE_CYCLES |",
+             f"| of which vector ALU (MFMA included) | {share('SQ_ACTIVE_INST_VALU')} | SQ_ACTIVE_INST_VALU / SQ_WAVE_CYCLES |",
+             f"| of which LDS | {share('SQ_ACTIVE_INST_LDS')} | SQ_ACTIVE_INST_LDS / SQ_WAVE_CYCLES |",
+             f"| waiting for its next instruction to issue | {share('SQ_WAIT_INST_ANY')} | SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES |",
+             f"| of which an LDS instruction | {share('SQ_WAIT_INST_LDS')} | SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES |",
+             f"| waiting for anything else (wait counts, barrier) | {share('SQ_WAIT_ANY')} | SQ_WAIT_ANY / SQ_WAVE_CYCLES |", ""]
+    out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}.stalls.md")
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "--mfma":
         mfma_summary(*sys.argv[2:4])
+    elif sys.argv[1] == "--stalls":
+        stall_summary(*sys.argv[2:4])
     else:
         main(*sys.argv[1:5])
