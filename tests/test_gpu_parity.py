@@ -331,6 +331,23 @@ def test_long_contexts_sampled(lib, decode_split):
     compare(out, ref, rows=rows, label=f"long contexts sampled {len(rows)} rows")
 
 
+@pytest.mark.parametrize("splits", [(0, 0), (64, 64)])
+def test_many_requests(lib, splits):
+    """A thousand requests in one step: 1,000 decode rows at 0-600 cached tokens and 8
+    short chunks, so the work list, the merge list and the partial slots are large (with
+    64-key splits, several thousand merged rows). Every decode row and sampled chunk rows
+    against the oracle."""
+    g = I.rng(13, 79)
+    seqs = [I.Seq(1, int(g.integers(0, 601)), i) for i in range(1000)]
+    seqs += [I.Seq(int(g.integers(2, 100)), int(g.integers(0, 2000)), 1000 + i) for i in range(8)]
+    spec = I.StepSpec("many-requests", seqs)
+    print(f"many requests: {len(seqs)} requests, {spec.n_rows} rows, splits {splits}", flush=True)
+    data, ds = run_step(lib, spec, 13, splits=splits)
+    rows = sample_rows(spec, I.rng(13, 80))
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows,
+            label=f"many requests, splits {splits}, {len(rows)} rows")
+
+
 @pytest.mark.parametrize("case", ["pressure-decode", "long", "tiny"])
 def test_decode_only_steps(lib, case):
     """Steps of decode rows only take even key pieces, about one item per CU: the 48
