@@ -241,3 +241,22 @@ def test_decode_only_steps_take_even_pieces_about_one_per_cu(num_cus):
     finally:
         ppas.set_split_keys(0, 0)
     assert ((fixed[:, 7] - fixed[:, 6]) <= 4096).all() and (fixed[:, 6] % 4096 == 0).all()
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No fallback: a copy of the package without libppas.so refuses to import its
+    binding (and the device-step module built on it)."""
+    import shutil
+    import subprocess
+    import sys
+    src = os.path.dirname(ppas.__file__)
+    dst = tmp_path / "paper_2608_15171_amd"
+    dst.mkdir()
+    for name in os.listdir(src):
+        if name.endswith(".py"):
+            shutil.copy(os.path.join(src, name), dst / name)
+    for mod in ("paper_2608_15171_amd.ppas", "paper_2608_15171_amd.step"):
+        r = subprocess.run([sys.executable, "-c", f"import {mod}"], cwd=tmp_path, capture_output=True, text=True,
+                           env={**os.environ, "PYTHONPATH": str(tmp_path)}, timeout=120)
+        assert r.returncode != 0, mod
+        assert "ImportError" in r.stderr and "libppas.so is missing" in r.stderr, r.stderr[-2000:]
