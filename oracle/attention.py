@@ -21,6 +21,11 @@ reference reads the logical, unpaged keys of each request.
 For each request s, KV head g, query head h in g's group and row i:
     l_j = scale * sum_d Q[qs+i, h, d] * K_s[j, g, d]      for j = 0..c+i
     O[qs+i, h, :] = sum_j exp(l_j - max l) V_s[j, g, :] / sum_j exp(l_j - max l)
+
+On request, the same weights also give A[qs+i, h, :] = sum_j w_j |V_s[j, g, :]|
+(w_j the normalised softmax weights): the weighted mean of the values' magnitudes,
+which bounds how far rounding the weights can move O (a test bound, not part of
+the attention).
 """
 from __future__ import annotations
 
@@ -42,8 +47,9 @@ def logical_kv(hist_bits, new_bits) -> np.ndarray:
     return np.concatenate(parts, axis=0)
 
 
-def _attend(qf, kf, vf, pos, scale):
-    """qf [r, G, D]; kf, vf [nk, D]; pos [r] positions; returns [r, G, D].
+def _attend(qf, kf, vf, pos, scale, with_abs=False):
+    """qf [r, G, D]; kf, vf [nk, D]; pos [r] positions; returns [r, G, D] (and the
+    weighted mean of |V| under the same weights when with_abs).
     Row i sees keys 0..pos[i]."""
     r, G, D = qf.shape
     logits = scale * (qf.reshape(r * G, D) @ kf.T).reshape(r, G, -1)
@@ -51,23 +57,28 @@ def _attend(qf, kf, vf, pos, scale):
     logits[np.broadcast_to(hidden[:, None, :], logits.shape)] = -np.inf
     m = logits.max(axis=-1, keepdims=True)
     w = np.exp(logits - m)
-    o = (w.reshape(r * G, -1) @ vf).reshape(r, G, D)
-    return o / w.sum(axis=-1)[..., None]
+    den = w.sum(axis=-1)[..., None]
+    o = (w.reshape(r * G, -1) @ vf).reshape(r, G, D) / den
+    if not with_abs:
+        return o
+    return o, (w.reshape(r * G, -1) @ np.abs(vf)).reshape(r, G, D) / den
 
 
 def mixed_step_attention(q_bits, desc, k_seq, v_seq, scale: float, n_kv_heads: int,
-                         rows=None, block_elems: int = 1 << 25) -> np.ndarray:
+                         rows=None, block_elems: int = 1 << 25, with_abs: bool = False):
     """Attention outputs of one mixed step.
 
     q_bits: uint16 bf16 [T, Hq, D]; desc: int [S, 3] of (query_start, n_query, cached_len);
     k_seq / v_seq: per request uint16 bf16 [cached_len + n_query, Hkv, D] (logical order).
     rows: optional iterable of row indices in [0, T); only those rows are computed and
-    the others are NaN. Returns float64 [T, Hq, D].
+    the others are NaN. Returns float64 [T, Hq, D]; with with_abs, the pair (O, A) of
+    the outputs and the weighted means of |V| (module docstring).
     """
     q_bits = np.asarray(q_bits, dtype=np.uint16)
     T, Hq, D = q_bits.shape
     G = Hq // n_kv_heads
     out = np.full((T, Hq, D), np.nan)
+    absv = np.full((T, Hq, D), np.nan) if with_abs else None
     want = None if rows is None else np.zeros(T, dtype=bool)
     if want is not None:
         want[np.asarray(list(rows), dtype=np.int64)] = True
@@ -90,16 +101,25 @@ def mixed_step_attention(q_bits, desc, k_seq, v_seq, scale: float, n_kv_heads: i
                 blk = local[start:start + rb]
                 nk = c + int(blk[-1]) + 1          # keys needed by the last row of the block
                 qf = bf16_to_f64(q_bits[qs + blk, hs, :])
-                out[qs + blk, hs, :] = _attend(qf, K[:nk, g, :], V[:nk, g, :], c + blk, scale)
+                res = _attend(qf, K[:nk, g, :], V[:nk, g, :], c + blk, scale, with_abs)
+                if with_abs:
+                    out[qs + blk, hs, :], absv[qs + blk, hs, :] = res
+                else:
+                    out[qs + blk, hs, :] = res
                 start += blk.size
-    return out
+    return (out, absv) if with_abs else out
 
 
-def step_attention_from_data(data, scale: float, rows=None) -> np.ndarray:
-    """Convenience wrapper over a StepData-like object (q, k_new, v_new, k_hist, v_hist, desc)."""
+def step_attention_from_data(data, scale: float, rows=None, with_abs: bool = False):
+    """The attention of a step given as a StepData-like object: q and the step's new
+    rows k_new / v_new [T, Hkv, D] (row query_start + i of request s is its position
+    cached_len + i), each request's cached history k_hist[s] / v_hist[s] (positions
+    0..cached_len-1), and desc. Request s's logical keys are its history followed by
+    its new rows qs..qs+n-1."""
     ks, vs = [], []
     for s in range(len(data.desc)):
         qs, n, _ = (int(x) for x in data.desc[s])
         ks.append(logical_kv(data.k_hist[s], data.k_new[qs:qs + n]))
         vs.append(logical_kv(data.v_hist[s], data.v_new[qs:qs + n]))
-    return mixed_step_attention(data.q, data.desc, ks, vs, scale, data.k_new.shape[1], rows=rows)
+    return mixed_step_attention(data.q, data.desc, ks, vs, scale, data.k_new.shape[1], rows=rows,
+                                with_abs=with_abs)

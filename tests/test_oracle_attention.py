@@ -33,13 +33,10 @@ def make(spec, seed):
     return I.make_step_data(spec, seed)
 
 
-def run(data, scale, mod=OA, rows=None):
-    ks, vs = [], []
-    for s in range(len(data.desc)):
-        qs, n, _ = (int(x) for x in data.desc[s])
-        ks.append(mod.logical_kv(data.k_hist[s], data.k_new[qs:qs + n]))
-        vs.append(mod.logical_kv(data.v_hist[s], data.v_new[qs:qs + n]))
-    return mod.mixed_step_attention(data.q, data.desc, ks, vs, scale, data.k_new.shape[1], rows=rows)
+def run(data, scale, mod=OA, rows=None, with_abs=False):
+    """The oracle's entry point for a step (the one the GPU tests, smoke() and the bench
+    call), so every pin below also covers how it assembles each request's keys."""
+    return mod.step_attention_from_data(data, scale, rows=rows, with_abs=with_abs)
 
 
 # ---------------------------------------------------------------- brute force
@@ -50,13 +47,15 @@ def bf16_scalar(b) -> float:
     return struct.unpack(">f", bytes([b >> 8, b & 0xFF, 0, 0]))[0]
 
 
-def brute_force(data, scale):
-    """Scalar loops with math.fsum; shares nothing with the oracle's NumPy code."""
+def brute_force(data, scale, with_abs=False):
+    """Scalar loops with math.fsum; shares nothing with the oracle's NumPy code. With
+    with_abs also the weighted mean of |V| under the same weights."""
     f64 = bf16_scalar
     T, Hq, D = data.q.shape
     Hkv = data.k_new.shape[1]
     G = Hq // Hkv
     out = np.zeros((T, Hq, D))
+    absv = np.zeros((T, Hq, D))
     for s in range(len(data.desc)):
         qs, n, c = (int(x) for x in data.desc[s])
         K = [[[float(f64(data.k_hist[s][j, g, d])) for d in range(D)] for g in range(Hkv)] for j in range(c)]
@@ -75,7 +74,8 @@ def brute_force(data, scale):
                 den = math.fsum(w)
                 for d in range(D):
                     out[qs + i, h, d] = math.fsum(w[j] * V[j][g][d] for j in range(p + 1)) / den
-    return out
+                    absv[qs + i, h, d] = math.fsum(w[j] * abs(V[j][g][d]) for j in range(p + 1)) / den
+    return (out, absv) if with_abs else out
 
 
 def tiny_spec(seed):
@@ -88,7 +88,22 @@ def tiny_spec(seed):
 @pytest.mark.parametrize("seed", range(6))
 def test_bruteforce_tiny(seed):
     data = make(tiny_spec(seed), seed)
-    np.testing.assert_allclose(run(data, 0.37), brute_force(data, 0.37), rtol=0, atol=1e-12)
+    o, a = run(data, 0.37, with_abs=True)
+    bo, ba = brute_force(data, 0.37, with_abs=True)
+    np.testing.assert_allclose(o, bo, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(a, ba, rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(run(data, 0.37), o)
+
+
+def test_entry_point_with_history_and_new_rows():
+    """step_attention_from_data on a step whose requests all have cached history and
+    new rows (prefill chunks and decodes, query_start > 0 for all but the first):
+    equal to the brute force, which reads history and new rows on its own."""
+    spec = I.StepSpec("hist", [I.Seq(1, 6, 0), I.Seq(4, 3, 1), I.Seq(3, 5, 2), I.Seq(1, 2, 3)],
+                      n_q_heads=4, n_kv_heads=2, head_dim=8)
+    data = make(spec, 31)
+    assert all(len(h) > 0 for h in data.k_hist)
+    np.testing.assert_allclose(OA.step_attention_from_data(data, 0.41), brute_force(data, 0.41), rtol=0, atol=1e-12)
 
 
 # ---------------------------------------------------------------- library pin
@@ -123,15 +138,17 @@ def test_zero_query_gives_prefix_mean():
     spec = I.StepSpec("z", [I.Seq(9, 5, 0), I.Seq(1, 11, 1)])
     data = make(spec, 3)
     data.q[:] = 0
-    out = run(data, SCALE128)
+    out, absv = run(data, SCALE128, with_abs=True)
     for s in range(2):
         qs, n, c = (int(x) for x in data.desc[s])
         V = np.concatenate([f64(data.v_hist[s]), f64(data.v_new[qs:qs + n])])
         csum = np.cumsum(V, axis=0)
+        asum = np.cumsum(np.abs(V), axis=0)
         for i in range(n):
             p = c + i
             want = csum[p] / (p + 1)                              # [Hkv, D]
             np.testing.assert_allclose(out[qs + i], np.repeat(want, 8, axis=0), rtol=0, atol=1e-13)
+            np.testing.assert_allclose(absv[qs + i], np.repeat(asum[p] / (p + 1), 8, axis=0), rtol=0, atol=1e-13)
 
 
 def test_equal_keys_give_prefix_mean():
@@ -149,8 +166,9 @@ def test_equal_keys_give_prefix_mean():
 def test_single_visible_key_returns_its_value_exactly():
     spec = I.StepSpec("one", [I.Seq(3, 0, 0)])
     data = make(spec, 5)
-    out = run(data, SCALE128)
+    out, absv = run(data, SCALE128, with_abs=True)
     assert np.array_equal(out[0], np.repeat(f64(data.v_new[0]), 8, axis=0))
+    assert np.array_equal(absv[0], np.abs(out[0]))
 
 
 def test_two_key_softmax_closed_form():
@@ -306,10 +324,19 @@ MUTANTS = {
     "sees_one_future_key": ("np.arange(kf.shape[0])[None, :] > pos[:, None]", "np.arange(kf.shape[0])[None, :] > pos[:, None] + 1"),
     "interleaved_head_groups": ("hs = slice(g * G, (g + 1) * G)", "hs = slice(g, Hq, n_kv_heads)"),
     "missing_scale": ("logits = scale * (qf", "logits = (qf"),
-    "missing_normalisation": ("return o / w.sum(axis=-1)[..., None]", "return o"),
+    "missing_normalisation": ("@ vf).reshape(r, G, D) / den", "@ vf).reshape(r, G, D)"),
     "history_after_new": ("parts.insert(0, np.asarray(hist_bits, dtype=np.uint16))", "parts.append(np.asarray(hist_bits, dtype=np.uint16))"),
-    "positions_from_zero": ("_attend(qf, K[:nk, g, :], V[:nk, g, :], c + blk, scale)", "_attend(qf, K[:nk, g, :], V[:nk, g, :], blk, scale)"),
+    "positions_from_zero": ("_attend(qf, K[:nk, g, :], V[:nk, g, :], c + blk, scale, with_abs)",
+                            "_attend(qf, K[:nk, g, :], V[:nk, g, :], blk, scale, with_abs)"),
     "bf16_low_half": ("(b.astype(np.uint32) << 16)", "(b.astype(np.uint32) << 15)"),
+    # the entry point's assembly of each request's keys and values
+    "entry_history_and_new_swapped": ("ks.append(logical_kv(data.k_hist[s], data.k_new[qs:qs + n]))",
+                                      "ks.append(logical_kv(data.k_new[qs:qs + n], data.k_hist[s]))"),
+    "entry_new_rows_from_zero": ("data.k_new[qs:qs + n]))", "data.k_new[0:n]))"),
+    "entry_values_from_keys": ("vs.append(logical_kv(data.v_hist[s], data.v_new[qs:qs + n]))",
+                               "vs.append(logical_kv(data.k_hist[s], data.k_new[qs:qs + n]))"),
+    # the weighted |V| output
+    "abs_of_signed_values": ("@ np.abs(vf)", "@ vf"),
 }
 
 
@@ -327,7 +354,9 @@ def pins_pass(mod) -> bool:
     try:
         for seed in range(3):
             d = make(tiny_spec(seed), seed)
-            if not np.allclose(run(d, 0.37, mod), brute_force(d, 0.37), rtol=0, atol=1e-12):
+            o, a = run(d, 0.37, mod, with_abs=True)
+            bo, ba = brute_force(d, 0.37, with_abs=True)
+            if not (np.allclose(o, bo, rtol=0, atol=1e-12) and np.allclose(a, ba, rtol=0, atol=1e-12)):
                 return False
         spec = I.random_small_step(1, max_seqs=4, max_n=40, max_c=90)
         d = make(spec, 1)
