@@ -9,11 +9,14 @@ table); they are resident in HBM before timing starts. The KV pools rotate over
 several device copies so that no timed step finds its keys in the 256 MB
 Infinity Cache from the previous step.
 
-Prints ONE JSON line. `value` is the algorithmic attention TFLOP/s of the whole
-step (FLOP = 4 * head_dim * n_q_heads * visible (row, key) pairs, softmax not
-counted). `roofline` describes the packed attention kernel, timed with HIP
-events recorded around its launch on its own stream. `cpu_baseline` times the
-CPU oracle on a bounded sample of the same step's rows.
+Prints ONE JSON line. By default the line is the 16,384-token chunk (the
+MBT=16384 step, where prefill work peaks) with the decode-heavy pressure step as
+a `secondary` record timed in the same run. `value` is the algorithmic
+attention TFLOP/s of the whole step (FLOP = 4 * head_dim * n_q_heads * visible
+(row, key) pairs, softmax not counted). `roofline` describes the packed
+attention kernel, timed with the HIP events its launch records on its own
+stream. `cpu_baseline` times the CPU oracle on a bounded sample of the same
+step's rows, with the BLAS pools set to the cores the process may use.
 """
 from __future__ import annotations
 
@@ -65,11 +68,26 @@ def measured_traffic(workload: str, kernel: str = "attn_step_kernel"):
     return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
 
 
-def cpu_baseline(data, scale, budget_s: float):
-    """Time the oracle on a bounded sample of the step's rows; returns the JSON object."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
+def host_cores() -> int:
+    """Cores this process may run on (its affinity mask), not the machine's count."""
+    return len(os.sched_getaffinity(0))
 
+
+def cpu_baseline(data, scale, budget_s: float):
+    """Time the oracle on a bounded sample of the step's rows, with the BLAS thread
+    pools set to the cores this process may use; returns the JSON object."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    cores = host_cores()
+    with threadpool_limits(limits=cores, user_api="blas"):
+        rec, rows, ref = _cpu_baseline(data, scale, budget_s)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    rec["cores"] = cores
+    rec["blas_threads_default"] = int(threads)
+    return rec, rows, ref
+
+
+def _cpu_baseline(data, scale, budget_s: float):
     import oracle.attention as OA
     spec = data.spec
     desc = data.desc
@@ -100,9 +118,8 @@ def cpu_baseline(data, scale, budget_s: float):
         if dt >= budget_s / 4 or frac >= 1.0:
             break
         frac = min(1.0, frac * max(2.0, budget_s / 2 / max(dt, 1e-3)))
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
     f = flop(rows)
-    rec = {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+    rec = {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": 0, "kind": "oracle",
            "sample": f"{len(rows)} of {spec.n_rows} query rows (every decode row and the last "
                      f"{frac:.2%} of each prefill chunk), all 16 heads, fp64 NumPy; {f:.3e} FLOP in {dt:.1f} s"}
     return rec, rows, ref
@@ -149,7 +166,7 @@ def run_trace_workload(args):
     big = max(range(len(setup.steps)), key=lambda i: setup.steps[i].spec.n_rows)
     print(f"trace: {len(setup.steps)} steps x {args.layers} layers, {len(setup.requests)} requests",
           file=sys.stderr, flush=True)
-    res = TR.run(setup, banks, args.layers,
+    res = TR.run(setup, banks, args.layers, check=[(big, 0)],
                  progress=lambda i, n: print(f"step {i}/{n}", file=sys.stderr, flush=True))
     t_attn = res["attn_ms_total"] * 1e-3
     rec = {
@@ -173,6 +190,7 @@ def run_trace_workload(args):
                    "heads": "16q/2kv", "head_dim": 128, "page_size": 16},
         "trace": {"attention_ms_total": round(res["attn_ms_total"], 3),
                   "kv_append_ms_total": round(res["kv_append_ms_total"], 3),
+                  "input_gather_ms_total": round(res["gather_ms_total"], 3),
                   "wall_ms": round(res["wall_ms"], 1), "attn_launches": res["launches"],
                   "flop_total": res["flops"], "decode_kv_bytes_total": res["decode_kv_bytes"],
                   "roofline_ms": round(max(res["flops"] / (PEAK_TFLOPS * 1e12),
@@ -184,9 +202,11 @@ def run_trace_workload(args):
     }
     if not args.no_cpu_baseline:
         data = TR.oracle_inputs(setup, banks, big, 0)
-        cb = cpu_baseline(data, 1.0 / math.sqrt(128.0), args.cpu_seconds)
-        cb[0]["sample"] = "largest step of the trace, layer 0: " + cb[0]["sample"]
-        rec["cpu_baseline"] = cb[0]
+        cb, rows, ref = cpu_baseline(data, 1.0 / math.sqrt(128.0), args.cpu_seconds)
+        cb["sample"] = "largest step of the trace, layer 0: " + cb["sample"]
+        rec["cpu_baseline"] = cb
+        rec["parity"] = parity_summary(res["checks"][(big, 0)].astype(np.float64), ref, rows)
+        rec["parity"]["step"] = big
     print(json.dumps(rec), flush=True)
 
 
@@ -218,9 +238,7 @@ def run_rope_workload(args, cfg):
     def timed(fn):
         ev = [(hip.create(), hip.create()) for _ in range(K)]
         for i in range(K):
-            ppas.set_profile_events(*ev[i])
-            fn(i)
-            ppas.set_profile_events(None, None)
+            fn(i, ppas.events(*ev[i]))
         torch.cuda.synchronize()
         t = [hip.elapsed_ms(a, b) * 1e3 for a, b in ev]
         for a, b in ev:
@@ -228,12 +246,16 @@ def run_rope_workload(args, cfg):
             hip.destroy(b)
         return t
 
-    rope = lambda i: ds.rope_append(theta, validate=False)       # noqa: E731  (rotates q again: norms kept)
-    plain = lambda i: ds.append(validate=False)                  # noqa: E731
+    plan = ds.plan(validate=False)
+    # (rotates q again each call: norms are kept)
+    rope = lambda i, ev=None: plan.rope_kv_append(theta, ds.q, ds.k_pages, ds.v_pages, ds.k_new, ds.v_new,  # noqa: E731
+                                                  ds.bt, ev)
+    plain = lambda i, ev=None: plan.kv_append(ds.k_pages, ds.v_pages, ds.k_new, ds.v_new, ds.bt, ev)  # noqa: E731
     W = warm_up(rope, args)
     t_rope = timed(rope)
     warm_up(plain, args)
     t_plain = timed(plain)
+    plan.close()
     us, us_plain = float(np.median(t_rope)), float(np.median(t_plain))
     T, D = spec.n_rows, spec.head_dim
     B = float(T * (2 * spec.n_q_heads * D * 2 + 2 * 2 * spec.n_kv_heads * D * 2))
@@ -401,50 +423,22 @@ def run_chunks_workload(args):
     print(json.dumps(rec), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed warm-up steps; default: as many as fill --warmup-seconds")
-    ap.add_argument("--warmup-seconds", type=float, default=0.25)
-    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mbt2048")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--layers", type=int, default=36, help="trace workload: layers")
-    ap.add_argument("--trace-mode", choices=["ppas", "fixed"], default="ppas", help="trace workload: budget policy")
-    ap.add_argument("--trace-mbt", type=int, default=16384, help="trace workload: global token budget")
-    ap.add_argument("--prompt", type=int, default=16384, help="chunks workload: prompt tokens")
-    ap.add_argument("--chunk", type=int, default=2048, help="chunks workload: tokens per chunk")
-    ap.add_argument("--rope-theta", type=float, default=1e6, help="rope workloads: rotary base")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
-              "multi-GPU mode (a step shards by request or by KV head with no exchange, which is not built)",
-              file=sys.stderr)
-        sys.exit(2)
-
+def measure_step(args, workload: str, with_cpu: bool):
+    """One single-step workload: K timed whole steps (plan + page write + attention +
+    merge), the kernels' own times from the events their launches record, the oracle
+    on a bounded sample beside it. Returns the JSON record."""
     import numpy as np
     import torch
 
     from paper_2608_15171_amd import inputs as I
     from paper_2608_15171_amd import metrics as M
     from paper_2608_15171_amd import ppas
+    from paper_2608_15171_amd.hip_events import HipEvents
     from paper_2608_15171_amd.step import DeviceStep
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    if args.workload == "trace":
-        return run_trace_workload(args)
-    if args.workload == "chunks":
-        return run_chunks_workload(args)
-    if args.workload == "trace-latency":
-        return run_trace_latency_workload(args)
-    if isinstance(WORKLOADS[args.workload], tuple):
-        return run_rope_workload(args, WORKLOADS[args.workload][1])
-    key = WORKLOADS[args.workload]
+    key = WORKLOADS[workload]
     spec = (I.CONFIGS[key] if isinstance(key, int) else I.DIAGNOSTICS[key])(args.seed)
+    print(f"bench: {workload} ({spec.name}, {spec.n_rows} rows)", file=sys.stderr, flush=True)
     data = I.make_step_data(spec, args.seed)
     bt, npages = I.make_block_table(spec, args.seed, permute=True)
     ds = DeviceStep(data, bt, npages)
@@ -452,47 +446,50 @@ def main():
     pool_bytes = ds.k_pages.numel() * 2 * 2
     copies = max(2, min(8, math.ceil(1.0e9 / pool_bytes) + 1))
     pools = [(ds.k_pages, ds.v_pages)] + [(ds.k_pages.clone(), ds.v_pages.clone()) for _ in range(copies - 1)]
+    probe = ds.plan()
+    has_merge = probe.info.n_merge > 0
+    tile = int(probe.info.tile_positions)
+    n_items = int(probe.info.n_items)
+    probe.close()
     torch.cuda.synchronize()
 
-    from paper_2608_15171_amd.hip_events import HipEvents
     hip = HipEvents()
-    K, W = args.steps, args.warmup
-    ev = [(hip.create(), hip.create()) for _ in range(K)]
+    K = args.steps
+    ev = [tuple(hip.create() for _ in range(4 if has_merge else 2)) for _ in range(K)]
     ea = [(hip.create(), hip.create()) for _ in range(K)]
 
-    # In the timed steps only the attention kernel's launch records events (its
-    # duration feeds the roofline); the append is timed in a pass of its own after
-    # them, because every extra event in the queue also adds to the step's wall time.
-    def one_step(i, timed):
+    # A step: plan (validation, work list, page-write list), the page write, the
+    # attention launch and the split merge. In the timed steps only the attention
+    # and merge launches record events (their durations feed the roofline); the
+    # page write is timed in a pass of its own afterwards, because every extra
+    # event also adds to the step's wall time.
+    def one_step(i, events=None, app_events=None):
         ds.k_pages, ds.v_pages = pools[i % copies]
-        ds.append()
-        if timed:
-            ppas.set_profile_events(*ev[i])
-        ds.attend()
-        if timed:
-            ppas.set_profile_events(None, None)
+        plan = ds.plan()
+        ds.append(plan=plan, events=app_events)
+        ds.attend(plan=plan, events=events)
+        plan.close()
 
-    W = warm_up(lambda i: one_step(i, False), args)
+    W = warm_up(lambda i: one_step(i), args)
     t0 = time.perf_counter()
     for i in range(K):
-        one_step(i, True)
+        one_step(i, events=ppas.events(*ev[i]))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(K):
-        ds.k_pages, ds.v_pages = pools[i % copies]
-        ppas.set_profile_events(*ea[i])
-        ds.append()
-        ppas.set_profile_events(None, None)
-        ds.attend()
+        one_step(i, app_events=ppas.events(*ea[i]))
     torch.cuda.synchronize()
 
     ms_step = (t1 - t0) / K * 1e3
-    attn_ms = [hip.elapsed_ms(a, b) for a, b in ev]
+    attn_ms = [hip.elapsed_ms(e[0], e[1]) for e in ev]
+    merge_ms = [hip.elapsed_ms(e[2], e[3]) for e in ev] if has_merge else [0.0] * K
+    span_ms = [hip.elapsed_ms(e[0], e[3]) for e in ev] if has_merge else attn_ms
     app_ms = [hip.elapsed_ms(a, b) for a, b in ea]
-    for a, b in ev + ea:
-        hip.destroy(a)
-        hip.destroy(b)
+    for e in ev + ea:
+        for x in e:
+            hip.destroy(x)
     k_ms = float(np.mean(attn_ms))
+    span = float(np.mean(span_ms))
 
     F = M.flops(spec)
     B = M.attn_bytes(spec)
@@ -500,8 +497,10 @@ def main():
     bound = "mfma" if t_flop >= t_byte else "hbm"
     if bound == "mfma":
         achieved, peak, unit = F / (k_ms * 1e-3) / 1e12, PEAK_TFLOPS, "TFLOP/s"
+        step_attn = F / (span * 1e-3) / 1e12
     else:
         achieved, peak, unit = B / (k_ms * 1e-3) / 1e9, PEAK_GBPS, "GB/s"
+        step_attn = B / (span * 1e-3) / 1e9
 
     rec = {
         "metric": METRIC,
@@ -524,18 +523,24 @@ def main():
                         f"{[(s.n_query, s.cached_len) for s in spec.seqs if s.n_query > 1]} (n_query, cached_len) chunks",
             "query_rows": spec.n_rows,
             "kv_tokens": int(spec.kv_lens().sum()),
-            "heads": f"{spec.n_q_heads}q/{spec.n_kv_heads}kv", "head_dim": 128, "page_size": 16, "block_table": "seeded permutation",
-            "kv_pool_copies_rotated": copies,
+            "heads": f"{spec.n_q_heads}q/{spec.n_kv_heads}kv", "head_dim": 128, "page_size": 16,
+            "block_table": "seeded permutation", "kv_pool_copies_rotated": copies,
+            "tile_positions": tile, "workgroups": n_items,
         },
         "roofline": {
             "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": measured_traffic(args.workload),
+            "frac": round(achieved / peak, 4), "traffic": measured_traffic(workload),
             "kernel": "attn_step_kernel", "kernel_us": round(k_ms * 1e3, 2),
             "per_launch": {"flop": F, "bytes": B},
         },
         "breakdown": {
             "attn_kernel_us": round(k_ms * 1e3, 2),
             "attn_kernel_us_min": round(float(np.min(attn_ms)) * 1e3, 2),
+            "merge_kernel_us": round(float(np.mean(merge_ms)) * 1e3, 2),
+            # from the attention launch's start to the merge launch's end: the whole
+            # attention of the step, dispatch gap included
+            "attn_with_merge_us": round(span * 1e3, 2),
+            "attn_with_merge_frac": round(step_attn / peak, 4),
             "kv_append_us": round(float(np.mean(app_ms)) * 1e3, 2),
             "tflops_in_kernel": round(F / (k_ms * 1e-3) / 1e12, 2),
             "mfma_frac": round(F / (k_ms * 1e-3) / 1e12 / PEAK_TFLOPS, 4),
@@ -546,9 +551,56 @@ def main():
             "step_roofline_us": round(max(t_flop, t_byte) * 1e6, 2),
         },
     }
-    if not args.no_cpu_baseline:
+    if with_cpu:
         rec["cpu_baseline"], rows, ref = cpu_baseline(data, ds.shape.scale, args.cpu_seconds)
         rec["parity"] = parity_summary(ds.out_f64(), ref, rows)
+    return rec
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed warm-up steps; default: as many as fill --warmup-seconds")
+    ap.add_argument("--warmup-seconds", type=float, default=0.25)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mbt16384")
+    ap.add_argument("--secondary", choices=sorted(k for k, v in WORKLOADS.items() if v is not None
+                                                  and not isinstance(v, tuple)) + ["none"], default="pressure",
+                    help="a second single-step workload timed in the same run and reported in the same line")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=36, help="trace workload: layers")
+    ap.add_argument("--trace-mode", choices=["ppas", "fixed"], default="ppas", help="trace workload: budget policy")
+    ap.add_argument("--trace-mbt", type=int, default=16384, help="trace workload: global token budget")
+    ap.add_argument("--prompt", type=int, default=16384, help="chunks workload: prompt tokens")
+    ap.add_argument("--chunk", type=int, default=2048, help="chunks workload: tokens per chunk")
+    ap.add_argument("--rope-theta", type=float, default=1e6, help="rope workloads: rotary base")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
+              "multi-GPU mode (a step shards by request or by KV head with no exchange, which is not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    if args.workload == "trace":
+        return run_trace_workload(args)
+    if args.workload == "chunks":
+        return run_chunks_workload(args)
+    if args.workload == "trace-latency":
+        return run_trace_latency_workload(args)
+    if isinstance(WORKLOADS[args.workload], tuple):
+        return run_rope_workload(args, WORKLOADS[args.workload][1])
+    rec = measure_step(args, args.workload, not args.no_cpu_baseline)
+    if args.secondary != "none" and args.secondary != args.workload:
+        sec = measure_step(args, args.secondary, not args.no_cpu_baseline)
+        rec["secondary"] = {k: sec[k] for k in ("config", "value", "unit", "ms_per_step", "steps", "warmup",
+                                                 "roofline", "breakdown", "cpu_baseline", "parity") if k in sec}
     print(json.dumps(rec), flush=True)
 
 

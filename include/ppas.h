@@ -16,8 +16,11 @@
  *   - bf16 means IEEE bfloat16 bit patterns (uint16 in memory).
  *   - Device pointers are HIP device memory on the current device; host pointers
  *     are ordinary host memory. The caller owns every buffer. The library
- *     allocates no device memory; it keeps a small pinned host staging ring for
- *     uploading its work list, released at process exit.
+ *     allocates no device memory; it keeps a pool of pinned host buffers that
+ *     hold its work lists (read by the kernels directly), released at process
+ *     exit.
+ *   - No state is shared between calls other than that pool: planning choices
+ *     and profiling events are arguments of the calls that use them.
  *   - All device work is enqueued on `hip_stream` (a hipStream_t, NULL = the
  *     null stream) and the call returns without synchronising the host. Calls
  *     on the same stream execute in order; append before attending.
@@ -79,18 +82,58 @@ typedef struct ppas_seq {
   int32_t cached_len;   /* tokens already in the cache before this step, >= 0 */
 } ppas_seq;
 
+/*
+ * Planning choices of one call (this library's own tuning, not a quantity of
+ * the paper). A zeroed struct, or NULL where a pointer is taken, selects the
+ * automatic choice for every field.
+ */
+typedef struct ppas_plan_opts {
+  int32_t prefill_split;    /* > 0: at most this many keys per prefill work item (rounded up to a
+                               multiple of 64); 0: about two prefill items per compute unit */
+  int32_t decode_split;     /* > 0: at most this many keys per decode work item (rounded up to a
+                               multiple of 32, capped at 16384); 0: automatic */
+  int32_t tile_positions;   /* 16 or 32: prefill tiles of that many positions (four- or eight-wave
+                               kernel); 0: chosen per step. Any other value is PPAS_EINVAL */
+  int32_t num_cus;          /* > 0: plan for a device with this many compute units; 0: the current
+                               device's count (ppas_plan_items: 256) */
+} ppas_plan_opts;
+
+/*
+ * HIP events (hipEvent_t handles created by the caller) that a call's kernel
+ * launches record as they start and end, so a kernel's own duration can be
+ * read with hipEventElapsedTime. Each pair is either both NULL (not recorded)
+ * or both set (PPAS_EINVAL otherwise).
+ *   start, stop              the call's main kernel: the packed attention
+ *                            launch, or the page-write launch of an append
+ *   merge_start, merge_stop  the split-merge launch of an attention call; not
+ *                            recorded when the call merges no split row
+ *                            (ppas_step_plan_info tells whether it does)
+ */
+typedef struct ppas_events {
+  void* start;
+  void* stop;
+  void* merge_start;
+  void* merge_stop;
+} ppas_events;
+
 /* Human-readable name of a status code. Never NULL; the string is static. */
 const char* ppas_status_string(ppas_status status);
 
 /*
  * Host-only check of a step description (no HIP call; usable without a GPU).
- * Checks the shape (PPAS_EUNSUPPORTED outside the compiled set, PPAS_EINVAL for
+ * The description is the one of a scheduler iteration in Section 2: each
+ * request contributes n_query new tokens (a prefill chunk, or one decode
+ * token) after cached_len tokens already in the KV cache, stored in pages
+ * (Section 7, PagedAttention) that the block table names. The checks
+ * themselves are this library's own:
+ * the shape (PPAS_EUNSUPPORTED outside the compiled set, PPAS_EINVAL for
  * non-positive sizes or a non-finite scale), each descriptor (n_query >= 1,
  * cached_len >= 0, contiguous query_start from 0, cached_len + n_query fitting in
  * int32: PPAS_EINVAL / PPAS_ERANGE), bt_stride >= ceil((cached_len+n_query)/16)
  * for every request (PPAS_EINVAL), and, when block_table_host is not NULL, that
  * every entry a request uses lies in [0, num_pages) (PPAS_ERANGE) and that no
- * two requests write the same (page, slot) in this step (PPAS_EINVAL).
+ * two requests write the same (page, slot) in this step (PPAS_EINVAL). The cost
+ * grows with the pages the requests use, not with num_pages.
  * n_seqs == 0 is a valid empty step.
  */
 ppas_status ppas_validate_step(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
@@ -103,10 +146,11 @@ ppas_status ppas_validate_step(const ppas_shape* shape, const ppas_seq* seqs, in
  * page = block_table[s][p / 16], slot = p % 16;
  *   k_pages[page][g][d / 8][slot][d % 8] = k_new[query_start + i][g][d]
  *   v_pages[page][g][:][slot] = v_new[query_start + i][g][:]   for every KV head g.
- * Bit-exact copies; no other byte of the pools is written. block_table_dev is
- * the device copy of the table; block_table_host (nullable) is a host copy used
- * only for validation (range and overlap checks are skipped when it is NULL,
- * and out-of-range device entries then give undefined results).
+ * Bit-exact copies; no other byte of the pools is written. One kernel launch
+ * for any number of requests. block_table_dev is the device copy of the table;
+ * block_table_host (nullable) is a host copy used only for validation (range
+ * and overlap checks are skipped when it is NULL, and out-of-range device
+ * entries then give undefined results).
  * Returns PPAS_OK or a validation / PPAS_EHIP status.
  */
 ppas_status ppas_kv_append(const ppas_shape* shape, void* k_pages, void* v_pages,
@@ -144,9 +188,11 @@ ppas_status ppas_rope_kv_append(const ppas_shape* shape, float rope_theta, void*
 
 /*
  * Device workspace that ppas_attn_step needs for this step description on the
- * current device: fp32 partial results of rows whose keys are split across
- * workgroups (at least 256 bytes). Depends only on the shape, the descriptors
- * and the device's compute-unit count. Returns 0 if the description is invalid.
+ * current device, with the automatic planning choices. This sizing call is the
+ * library's own (the paper describes no workspace): the workspace holds the
+ * fp32 partial results of rows whose keys are split across workgroups of the
+ * launch (at least 256 bytes). Depends only on the shape, the descriptors and
+ * the device's compute-unit count. Returns 0 if the description is invalid.
  */
 size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs);
 
@@ -164,12 +210,13 @@ size_t ppas_attn_workspace_bytes(const ppas_shape* shape, const ppas_seq* seqs, 
  * across workgroups are merged by a second, small launch.
  * workspace: device buffer of at least ppas_attn_workspace_bytes() bytes, owned
  * by the caller, not read before being written; it must not be used by another
- * call still in flight. The work list itself travels in pinned host memory the
- * library owns (a ring of eight staging buffers per device, read by the kernels
- * directly); a call waits on the device only when the buffer it would reuse is
- * still being read by a launch eight calls back. Because the work list is staged
- * per call, a call cannot be captured into a HIP graph and replayed. Calls from
- * several threads or on several streams are safe (each with its own workspace).
+ * call still in flight. The work list travels in pinned host memory from a pool
+ * the library owns, read by the kernels directly; a buffer of the pool is
+ * reused only after the launches that read it have completed. Because the work
+ * list is staged per call, a call cannot be captured into a HIP graph and
+ * replayed. Calls from several threads or on several streams are safe (each
+ * with its own workspace). Equivalent to creating a step plan with default
+ * options, ppas_attn_step_planned, and destroying the plan.
  * Returns PPAS_OK, a validation status, PPAS_ENOSPACE or PPAS_EHIP.
  */
 ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q,
@@ -180,49 +227,83 @@ ppas_status ppas_attn_step(const ppas_shape* shape, void* out, const void* q,
                            void* workspace, size_t workspace_bytes, void* hip_stream);
 
 /*
- * Work-list introspection for tests (host only, no HIP call). Plans the step for
- * a device with `num_cus` compute units and writes at most `capacity` items of 8
- * int32 each to `items_out` (kind, seq, kv_head, row0, pos0, npos, key_lo,
- * key_hi per item, in launch order; kind 0 = prefill tile, 1 = decode row).
- * Returns the number of items, or a negative ppas_status.
+ * Step plans. One scheduler iteration runs every decoder layer over the same
+ * batch of requests (Section 2: an iteration processes the batch's tokens
+ * through the model; Section 6.1 profiles one decoder block of it), so the
+ * host work of a step (validation, the attention work list, the page-write
+ * list) is the same for every layer. A plan holds that work once, for as many
+ * launches as the caller makes with it: ppas_kv_append_planned,
+ * ppas_rope_kv_append_planned and ppas_attn_step_planned then only launch
+ * kernels. The plan keeps the shape, the descriptors' work and bt_stride; each
+ * planned call takes the layer's device buffers and block table (same stride).
+ *
+ * ppas_step_plan_create validates as ppas_validate_step does (with the range
+ * and overlap checks when block_table_host is not NULL), plans with `opts`
+ * (NULL = automatic) for the current device, and stores the lists in pinned
+ * host memory from the library's pool. *plan receives the handle (NULL on
+ * error). Returns PPAS_OK, a validation status, PPAS_ERANGE for a step too
+ * large for the int32 work list, PPAS_EUNSUPPORTED without a gfx950 device, or
+ * PPAS_EHIP.
+ */
+typedef struct ppas_step_plan ppas_step_plan;
+
+ppas_status ppas_step_plan_create(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
+                                  const int32_t* block_table_host, int32_t bt_stride,
+                                  const ppas_plan_opts* opts, ppas_step_plan** plan);
+
+/* What a plan launches (host only). */
+typedef struct ppas_plan_info {
+  int32_t n_items;          /* workgroups of the packed attention launch */
+  int32_t n_merge;          /* split-merge items (0: no merge launch) */
+  int32_t tile_positions;   /* 16 or 32 */
+  int32_t n_append;         /* (request, page) workgroups of a page-write launch */
+  uint64_t workspace_bytes; /* workspace ppas_attn_step_planned needs */
+} ppas_plan_info;
+
+ppas_status ppas_step_plan_info(const ppas_step_plan* plan, ppas_plan_info* info);
+
+/* As ppas_kv_append, with the plan's descriptors and validation; events may be NULL. */
+ppas_status ppas_kv_append_planned(const ppas_step_plan* plan, void* k_pages, void* v_pages,
+                                   const void* k_new, const void* v_new,
+                                   const int32_t* block_table_dev, const ppas_events* events,
+                                   void* hip_stream);
+
+/* As ppas_rope_kv_append, with the plan's descriptors and validation; events may be NULL. */
+ppas_status ppas_rope_kv_append_planned(const ppas_step_plan* plan, float rope_theta, void* q,
+                                        void* k_pages, void* v_pages,
+                                        const void* k_new, const void* v_new,
+                                        const int32_t* block_table_dev, const ppas_events* events,
+                                        void* hip_stream);
+
+/*
+ * As ppas_attn_step, with the plan's descriptors, validation and work list
+ * (workspace of at least ppas_plan_info.workspace_bytes); events may be NULL.
+ * Calls with one plan may run on several streams at once, each with its own
+ * workspace.
+ */
+ppas_status ppas_attn_step_planned(const ppas_step_plan* plan, void* out, const void* q,
+                                   const void* k_pages, const void* v_pages,
+                                   const int32_t* block_table_dev,
+                                   void* workspace, size_t workspace_bytes,
+                                   const ppas_events* events, void* hip_stream);
+
+/*
+ * Release a plan (NULL is a no-op). Does not wait: the plan's pinned memory
+ * returns to the pool and is reused only after every launch made with the plan
+ * has completed.
+ */
+void ppas_step_plan_destroy(ppas_step_plan* plan);
+
+/*
+ * Work-list introspection for tests (host only, no HIP call). Plans the step
+ * with `opts` (NULL = automatic; num_cus 0 = 256 compute units) and writes at
+ * most `capacity` items of 8 int32 each to `items_out` (kind, seq, kv_head, row0,
+ * pos0, npos, key_lo, key_hi per item, in launch order; kind 0 = prefill tile,
+ * 1 = decode row). Returns the number of items, or a negative ppas_status
+ * (PPAS_EINVAL also for an invalid opts field).
  */
 int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
-                        int32_t num_cus, int32_t* items_out, int32_t capacity);
-
-/*
- * Planner tuning (process-wide; 0 restores the automatic choice). prefill_split
- * and decode_split cap the keys one workgroup processes for a prefill tile /
- * a decode row (rounded to multiples of 64 / 32). Affects plans made after the
- * call, including ppas_attn_workspace_bytes. Returns PPAS_EINVAL for negative
- * values.
- */
-ppas_status ppas_set_split_keys(int32_t prefill_split, int32_t decode_split);
-
-/*
- * Planner tuning (process-wide). The packed launch comes in two shapes: prefill
- * tiles of 16 positions on four-wave workgroups, or of 32 positions on
- * eight-wave workgroups (each staged K/V block then serves twice the rows). By
- * default (0) each step picks 32 only when its 32-position tiles reach two per
- * compute unit and decode rows are a small share of its work; 16 or 32 forces
- * the shape. Affects plans made after the call, including
- * ppas_attn_workspace_bytes and ppas_plan_items (whose npos then reaches 32).
- * Returns PPAS_EINVAL for any other value.
- */
-ppas_status ppas_set_tile_positions(int32_t tile_positions);
-
-/*
- * Profiling hook (process-wide). When both are non-NULL, the following calls
- * have their kernel launches record `start_event` when the kernel starts and
- * `stop_event` when it ends (hipEvent_t handles created by the caller;
- * hipExtLaunchKernel's events), so a kernel's own duration can be read with
- * hipEventElapsedTime: in ppas_attn_step the packed attention kernel (not the
- * split merge), in ppas_kv_append and ppas_rope_kv_append their page-write
- * kernel (start at the first launch, stop at the last when a call needs several
- * launches for over 64 requests). Pass NULLs to stop recording. The events are
- * re-recorded by every call; the caller owns and destroys them.
- * Returns PPAS_EINVAL if exactly one of them is NULL.
- */
-ppas_status ppas_set_profile_events(void* start_event, void* stop_event);
+                        const ppas_plan_opts* opts, int32_t* items_out, int32_t capacity);
 
 #ifdef __cplusplus
 }

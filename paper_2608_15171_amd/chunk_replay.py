@@ -70,28 +70,26 @@ class Replay:
 
     def run(self, chunk: int) -> list:
         """Prefill the whole prompt in chunks of `chunk` tokens; returns each chunk's
-        attention kernel time in ms (HIP events around the packed launch)."""
+        attention kernel time in ms (HIP events the packed launch records)."""
         import torch
         specs = chunk_specs(self.prompt, chunk)
-        need = max(ppas.attn_workspace_bytes(self.shape, s.descriptors()) for s in specs)
+        plans = [ppas.StepPlan(self.shape, s.descriptors(), self.bt_host) for s in specs]
+        need = max(p.workspace_bytes for p in plans)
         if self.ws.numel() < need:
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.q.device)
         evs = []
-        for s in specs:
+        for s, plan in zip(specs, plans):
             desc = s.descriptors()
             lo = int(desc[0, 2])
             hi = lo + int(desc[0, 1])
-            ppas.kv_append(self.shape, self.k_pages, self.v_pages, self.k[lo:hi], self.v[lo:hi], desc,
-                           self.bt, self.bt_host)
+            plan.kv_append(self.k_pages, self.v_pages, self.k[lo:hi], self.v[lo:hi], self.bt)
             e0, e1 = self.events.create(), self.events.create()
-            ppas.set_profile_events(e0, e1)
-            try:
-                ppas.attn_step(self.shape, self.out[lo:hi], self.q[lo:hi], self.k_pages, self.v_pages, desc,
-                               self.bt, self.ws, self.bt_host)
-            finally:
-                ppas.set_profile_events(None, None)
+            plan.attn_step(self.out[lo:hi], self.q[lo:hi], self.k_pages, self.v_pages, self.bt, self.ws,
+                           ppas.events(e0, e1))
             evs.append((e0, e1))
         torch.cuda.synchronize()
+        for plan in plans:
+            plan.close()
         ms = [self.events.elapsed_ms(a, b) for a, b in evs]
         for a, b in evs:
             self.events.destroy(a)

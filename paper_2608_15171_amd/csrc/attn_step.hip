@@ -725,7 +725,8 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
                             const int32_t* bt, int32_t bt_stride, int32_t hq, int32_t hkv, float scale,
                             const WorkItem* items, int n_items, const CombineItem* comb, int n_comb,
                             float2* part_ml, float* part_acc, int tile_pos, hipStream_t stream,
-                            hipEvent_t ev_start, hipEvent_t ev_stop) {
+                            hipEvent_t ev_start, hipEvent_t ev_stop, hipEvent_t ev_merge_start,
+                            hipEvent_t ev_merge_stop) {
   if (tile_pos != kTilePosSmall && tile_pos != kTilePosLarge) return hipErrorInvalidValue;
   if (n_items > 0) {
     StepArgs a;
@@ -755,8 +756,8 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
   }
   if (n_comb > 0) {
     const int ymax = tile_pos * kGroup / kCombineRowsPerBlock;
-    hipLaunchKernelGGL(combine_kernel, dim3(n_comb, ymax), dim3(kCombineThreads), 0, stream, comb, part_ml, part_acc,
-                       out, hq);
+    hipExtLaunchKernelGGL(combine_kernel, dim3(n_comb, ymax), dim3(kCombineThreads), 0, stream, ev_merge_start,
+                          ev_merge_stop, 0, comb, part_ml, part_acc, out, hq);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -1,6 +1,7 @@
 // Scatter a step's new K/V rows into the paged cache (bit copies).
 //
-// One workgroup per (request, touched page, KV head). The K page of one head is
+// One workgroup per (request, touched page, KV head); the (request, page) pairs
+// come from a list the host builds, so one launch covers any number of requests. The K page of one head is
 // 16 chunks of 8 features, each holding the 16 slots' 16-byte pieces: thread t
 // copies the piece (chunk t/16, slot t%16) when that slot is one of the step's
 // positions, so a workgroup's K stores are one contiguous 4 KB run. The V page
@@ -16,29 +17,25 @@
 
 namespace ppas {
 
-constexpr int kAppendMaxSeqs = 64;
-
 struct AppendArgs {
   uint16_t* kp;
   uint16_t* vp;
   const uint16_t* kn;
   const uint16_t* vn;
   const int32_t* bt;
-  int32_t bt_stride, hkv, n, seq_base;
-  int32_t blk_start[kAppendMaxSeqs + 1];   // prefix sums of touched pages per request
-  int32_t qs[kAppendMaxSeqs], nq[kAppendMaxSeqs], c[kAppendMaxSeqs];
+  const AppendItem* items;   // one per workgroup (x): request and logical page
+  int32_t bt_stride, hkv;
 };
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
-  const int blk = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
-  int s = 0;
-  while (s + 1 < a.n && a.blk_start[s + 1] <= blk) ++s;
-  const int c = a.c[s], nq = a.nq[s], qs = a.qs[s];
-  const int lpage = c / kPage + (blk - a.blk_start[s]);
+  const AppendItem it = a.items[blockIdx.x];
+  const int g = blockIdx.y, tid = threadIdx.x;
+  const int c = it.cached_len, nq = it.n_query, qs = it.query_start;
+  const int lpage = it.lpage;
   const int pos_lo = lpage * kPage;                       // position of slot 0 of this page
-  const int32_t page = a.bt[size_t(a.seq_base + s) * a.bt_stride + lpage];
+  const int32_t page = a.bt[size_t(it.seq) * a.bt_stride + lpage];
   const size_t base = (size_t(page) * a.hkv + g) * kPage * kHeadDim;
   const size_t row_stride = size_t(a.hkv) * kHeadDim;     // elements between new rows
 
@@ -81,39 +78,20 @@ __global__ __launch_bounds__(256) void kv_append_kernel(AppendArgs a) {
 }
 
 hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
-                            const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
+                            const AppendItem* items, int32_t n_items, const int32_t* bt, int32_t bt_stride,
                             int32_t hkv, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
-  for (int32_t s0 = 0; s0 < n_seqs; s0 += kAppendMaxSeqs) {
-    AppendArgs a;
-    a.kp = kp;
-    a.vp = vp;
-    a.kn = kn;
-    a.vn = vn;
-    a.bt = bt;
-    a.bt_stride = bt_stride;
-    a.hkv = hkv;
-    a.seq_base = s0;
-    a.n = 0;
-    int32_t blocks = 0;
-    for (int32_t s = s0; s < n_seqs && s < s0 + kAppendMaxSeqs; ++s) {
-      const int i = a.n++;
-      a.qs[i] = seqs[s].query_start;
-      a.nq[i] = seqs[s].n_query;
-      a.c[i] = seqs[s].cached_len;
-      a.blk_start[i] = blocks;
-      const int first = seqs[s].cached_len / kPage;
-      const int last = (seqs[s].cached_len + seqs[s].n_query - 1) / kPage;
-      blocks += last - first + 1;
-    }
-    a.blk_start[a.n] = blocks;
-    // profiling events (optional): the first launch records the start, the last one the stop
-    const bool last = s0 + kAppendMaxSeqs >= n_seqs;
-    hipExtLaunchKernelGGL(kv_append_kernel, dim3(blocks, hkv), dim3(256), 0, stream, s0 == 0 ? ev_start : nullptr,
-                          last ? ev_stop : nullptr, 0, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  if (n_items <= 0) return hipSuccess;
+  AppendArgs a;
+  a.kp = kp;
+  a.vp = vp;
+  a.kn = kn;
+  a.vn = vn;
+  a.bt = bt;
+  a.items = items;
+  a.bt_stride = bt_stride;
+  a.hkv = hkv;
+  hipExtLaunchKernelGGL(kv_append_kernel, dim3(n_items, hkv), dim3(256), 0, stream, ev_start, ev_stop, 0, a);
+  return hipGetLastError();
 }
 
 }  // namespace ppas

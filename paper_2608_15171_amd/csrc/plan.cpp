@@ -2,17 +2,12 @@
 #include "plan.h"
 
 #include <algorithm>
-#include <atomic>
 #include <cmath>
 #include <numeric>
 
 namespace ppas {
 
 namespace {
-std::atomic<int32_t> g_prefill_split{0};
-std::atomic<int32_t> g_decode_split{0};
-std::atomic<int32_t> g_tile_pos{0};
-
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // decode cost / prefill cost above which the two kinds are interleaved
@@ -36,13 +31,6 @@ constexpr double kLargeTileDecodeShare = PPAS_LARGE_TILE_DECODE_SHARE;
 #endif
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 }  // namespace
-
-void set_tile_positions(int32_t tile_pos) { g_tile_pos.store(tile_pos); }
-
-void set_split_keys(int32_t prefill, int32_t decode) {
-  g_prefill_split.store(prefill);
-  g_decode_split.store(decode);
-}
 
 ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
                      const int32_t* bt_host, int32_t bt_stride, bool check_overlap) {
@@ -77,17 +65,28 @@ ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_se
       if (row[j] < 0 || row[j] >= s.num_pages) return PPAS_ERANGE;
   }
   if (check_overlap) {
-    // no (page, slot) may be written by two requests of the same step
-    std::vector<uint16_t> used(size_t(s.num_pages), 0);   // bit per slot
+    // No (page, slot) may be written by two requests of the step. A request's new
+    // positions form one run of slots per page it touches; sorting those runs by
+    // (page, first slot) puts any two that share a page side by side, so the cost
+    // follows the pages the step writes, not the size of the pool.
+    struct Run {
+      int32_t page, lo, hi;   // slots lo..hi of the page
+    };
+    std::vector<Run> runs;
     for (int32_t i = 0; i < n_seqs; ++i) {
       const int32_t* row = bt_host + int64_t(i) * bt_stride;
-      for (int64_t p = seqs[i].cached_len; p < int64_t(seqs[i].cached_len) + seqs[i].n_query; ++p) {
-        const int32_t page = row[p / kPage];
-        const uint16_t bit = uint16_t(1u << (p % kPage));
-        if (used[page] & bit) return PPAS_EINVAL;
-        used[page] |= bit;
+      const int64_t end = int64_t(seqs[i].cached_len) + seqs[i].n_query;
+      for (int64_t p = seqs[i].cached_len; p < end;) {
+        const int64_t lp = p / kPage;
+        const int64_t stop = std::min(end, (lp + 1) * kPage);
+        runs.push_back(Run{row[lp], int32_t(p % kPage), int32_t((stop - 1) % kPage)});
+        p = stop;
       }
     }
+    std::sort(runs.begin(), runs.end(),
+              [](const Run& a, const Run& b) { return a.page != b.page ? a.page < b.page : a.lo < b.lo; });
+    for (size_t k = 1; k < runs.size(); ++k)
+      if (runs[k].page == runs[k - 1].page && runs[k].lo <= runs[k - 1].hi) return PPAS_EINVAL;
   }
   return PPAS_OK;
 }
@@ -102,7 +101,8 @@ struct Job {
 
 }  // namespace
 
-void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, Plan& plan) {
+void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, const PlanOpts& opts,
+               Plan& plan) {
   plan.items.clear();
   plan.combine.clear();
   plan.part_slots = 0;
@@ -135,7 +135,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   // 32-position tiles (two per CU before any key split) and decode rows are a
   // small share of the work (a workgroup then holds a whole CU, so a prefill
   // tile no longer shares its CU with a decode item).
-  int32_t tile = g_tile_pos.load();
+  int32_t tile = opts.tile_pos;
   if (tile != kTilePosSmall && tile != kTilePosLarge) {
     const int64_t small_keys = prefill_keys_for(kTilePosSmall);
     const bool big = large_tiles >= int64_t(2) * num_cus;
@@ -145,13 +145,13 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   plan.tile_pos = tile;
   const int64_t prefill_keys = prefill_keys_for(tile);
 
-  int64_t ksp = g_prefill_split.load();
+  int64_t ksp = opts.prefill_split;
   if (ksp <= 0) {
     const int64_t target = int64_t(PPAS_PREFILL_ITEMS_PER_CU) * num_cus;
     ksp = std::max<int64_t>(256, ceil_div(prefill_keys, target));
   }
   ksp = std::max<int64_t>(kPrefillBlock, ceil_div(ksp, kPrefillBlock) * kPrefillBlock);
-  int64_t ksd = g_decode_split.load();
+  int64_t ksd = opts.decode_split;
   if (ksd <= 0) {
     const int64_t target = int64_t(2) * num_cus;
     ksd = std::min<int64_t>(8192, std::max<int64_t>(512, ceil_div(decode_keys, target)));
@@ -179,7 +179,7 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   // (measured on 48 rows of 20k-30k keys: 190 us with ~one item per CU against
   // 205 us with about two per CU, ragged). A piece never exceeds the page-id
   // capacity of a decode item.
-  const bool decode_even = prefill_keys == 0 && decode_keys > 0 && g_decode_split.load() <= 0;
+  const bool decode_even = prefill_keys == 0 && decode_keys > 0 && opts.decode_split <= 0;
   auto piece_bounds = [&](int64_t kend, int64_t pos0, int kind) {
     std::vector<int64_t> b{0};
     if (kind == kKindDecode && decode_even) {
@@ -294,6 +294,17 @@ void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, in
   plan.off_ml = 0;
   plan.off_acc = align_up(size_t(plan.part_slots) * 8, 256);
   plan.total = std::max<size_t>(256, align_up(plan.off_acc + size_t(plan.part_slots) * kHeadDim * 4, 256));
+}
+
+void make_append_items(const ppas_seq* seqs, int32_t n_seqs, std::vector<AppendItem>& items) {
+  items.clear();
+  for (int32_t s = 0; s < n_seqs; ++s) {
+    const ppas_seq& q = seqs[s];
+    const int32_t first = q.cached_len / kPage;
+    const int32_t last = int32_t((int64_t(q.cached_len) + q.n_query - 1) / kPage);
+    for (int32_t lp = first; lp <= last; ++lp)
+      items.push_back(AppendItem{s, lp, q.cached_len, q.n_query, q.query_start, 0, 0, 0});
+  }
 }
 
 }  // namespace ppas

@@ -41,6 +41,22 @@ struct CombineItem {
 };
 static_assert(sizeof(CombineItem) == 32, "CombineItem is 32 bytes");
 
+// One workgroup of the page-write kernels: the new rows of request `seq` that fall
+// in its logical page `lpage` (positions lpage*16.. of the request), for every KV
+// head. The request's rows are query_start..query_start+n_query-1 at positions
+// cached_len..cached_len+n_query-1.
+struct AppendItem {
+  int32_t seq, lpage, cached_len, n_query, query_start, pad0, pad1, pad2;
+};
+static_assert(sizeof(AppendItem) == 32, "AppendItem is 32 bytes");
+
+// Per-call planning choices; zero selects the automatic one.
+struct PlanOpts {
+  int32_t prefill_split = 0;       // >0: keys per prefill work item at most (rounded up to 64)
+  int32_t decode_split = 0;        // >0: keys per decode work item at most (rounded up to 32)
+  int32_t tile_pos = 0;            // 16 or 32 forces the prefill tile shape
+};
+
 struct Plan {
   int tile_pos = kTilePosSmall;    // prefill tile positions, selects the kernel shape
   std::vector<WorkItem> items;     // in launch order
@@ -56,11 +72,10 @@ ppas_status validate(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_se
                      const int32_t* bt_host, int32_t bt_stride, bool check_overlap);
 
 // Builds the plan for a device with num_cus compute units. The step must already be valid.
-void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, Plan& plan);
+void make_plan(const ppas_shape& shape, const ppas_seq* seqs, int32_t n_seqs, int num_cus, const PlanOpts& opts,
+               Plan& plan);
 
-void set_split_keys(int32_t prefill, int32_t decode);
-
-// 0: choose the tile size per step; 16 or 32: force it.
-void set_tile_positions(int32_t tile_pos);
+// The page-write work of a valid step: one item per (request, touched logical page).
+void make_append_items(const ppas_seq* seqs, int32_t n_seqs, std::vector<AppendItem>& items);
 
 }  // namespace ppas

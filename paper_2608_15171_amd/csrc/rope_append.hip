@@ -7,7 +7,7 @@
 // p * theta^(-2i/128). Query rows are rotated in place; rotated keys go to the
 // pages exactly where the plain append puts keys; values are copied unrotated.
 //
-// One workgroup per (request, touched page): it covers up to 16 consecutive
+// One workgroup per (request, touched page), from a list the host builds: it covers up to 16 consecutive
 // positions of one request and all heads of those rows, so the cos/sin pairs of
 // its positions are computed once (16 x 64 entries in LDS) and shared by the 16
 // query heads and the KV heads. Angles are reduced in fp64 (whole turns
@@ -26,7 +26,6 @@
 
 namespace ppas {
 
-constexpr int kRopeMaxSeqs = 64;
 constexpr int kRopePairs = kHeadDim / 2;
 
 struct RopeArgs {
@@ -36,9 +35,8 @@ struct RopeArgs {
   const uint16_t* kn;
   const uint16_t* vn;
   const int32_t* bt;
-  int32_t bt_stride, hq, hkv, n, seq_base;
-  int32_t blk_start[kRopeMaxSeqs + 1];   // prefix sums of touched pages per request
-  int32_t qs[kRopeMaxSeqs], nq[kRopeMaxSeqs], c[kRopeMaxSeqs];
+  const AppendItem* items;               // one per workgroup: request and logical page
+  int32_t bt_stride, hq, hkv;
   double turns[kRopePairs];              // turns per position of pair i: theta^(-2i/128) / (2 pi)
 };
 
@@ -67,14 +65,13 @@ __device__ __forceinline__ void rotate8(u32x4& x, u32x4& y, const float2* cs) {
 
 __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
   __shared__ float2 cs[kPage][kRopePairs];
-  const int blk = blockIdx.x, tid = threadIdx.x;
-  int s = 0;
-  while (s + 1 < a.n && a.blk_start[s + 1] <= blk) ++s;
-  const int c = a.c[s], nq = a.nq[s], qs = a.qs[s];
-  const int lpage = c / kPage + (blk - a.blk_start[s]);
+  const AppendItem it = a.items[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int c = it.cached_len, nq = it.n_query, qs = it.query_start;
+  const int lpage = it.lpage;
   const int pos_lo = lpage * kPage;                                   // position of slot 0
   const int slot_lo = max(c - pos_lo, 0), slot_hi = min(c + nq - pos_lo, kPage);
-  const int32_t page = a.bt[size_t(a.seq_base + s) * a.bt_stride + lpage];
+  const int32_t page = a.bt[size_t(it.seq) * a.bt_stride + lpage];
 
   for (int e = tid; e < kPage * kRopePairs; e += blockDim.x) {
     const int slot = e / kRopePairs, i = e % kRopePairs;
@@ -141,41 +138,24 @@ __global__ __launch_bounds__(256) void rope_append_kernel(RopeArgs a) {
 }
 
 hipError_t launch_rope_append(uint16_t* q, uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
-                              const ppas_seq* seqs, int32_t n_seqs, const int32_t* bt, int32_t bt_stride,
+                              const AppendItem* items, int32_t n_items, const int32_t* bt, int32_t bt_stride,
                               int32_t hq, int32_t hkv, double theta, hipStream_t stream, hipEvent_t ev_start,
                               hipEvent_t ev_stop) {
+  if (n_items <= 0) return hipSuccess;
   RopeArgs a;
   for (int i = 0; i < kRopePairs; ++i) a.turns[i] = std::pow(theta, -2.0 * i / kHeadDim) / (2.0 * M_PI);
-  for (int32_t s0 = 0; s0 < n_seqs; s0 += kRopeMaxSeqs) {
-    a.q = q;
-    a.kp = kp;
-    a.vp = vp;
-    a.kn = kn;
-    a.vn = vn;
-    a.bt = bt;
-    a.bt_stride = bt_stride;
-    a.hq = hq;
-    a.hkv = hkv;
-    a.seq_base = s0;
-    a.n = 0;
-    int32_t blocks = 0;
-    for (int32_t s = s0; s < n_seqs && s < s0 + kRopeMaxSeqs; ++s) {
-      const int i = a.n++;
-      a.qs[i] = seqs[s].query_start;
-      a.nq[i] = seqs[s].n_query;
-      a.c[i] = seqs[s].cached_len;
-      a.blk_start[i] = blocks;
-      blocks += (seqs[s].cached_len + seqs[s].n_query - 1) / kPage - seqs[s].cached_len / kPage + 1;
-    }
-    a.blk_start[a.n] = blocks;
-    // profiling events (optional): the first launch records the start, the last one the stop
-    const bool last = s0 + kRopeMaxSeqs >= n_seqs;
-    hipExtLaunchKernelGGL(rope_append_kernel, dim3(blocks), dim3(256), 0, stream, s0 == 0 ? ev_start : nullptr,
-                          last ? ev_stop : nullptr, 0, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  a.q = q;
+  a.kp = kp;
+  a.vp = vp;
+  a.kn = kn;
+  a.vn = vn;
+  a.bt = bt;
+  a.items = items;
+  a.bt_stride = bt_stride;
+  a.hq = hq;
+  a.hkv = hkv;
+  hipExtLaunchKernelGGL(rope_append_kernel, dim3(n_items), dim3(256), 0, stream, ev_start, ev_stop, 0, a);
+  return hipGetLastError();
 }
 
 }  // namespace ppas

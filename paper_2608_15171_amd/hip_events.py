@@ -1,8 +1,8 @@
 """hipEvent_t handles through the HIP runtime already loaded in the process.
 
-The library records such events around its packed attention launch
-(ppas_set_profile_events), so the kernel's own duration can be read on the
-stream it was launched on. Import after torch (the binding does), so the name
+The library's launches record such events when a call passes them (the
+ppas_events argument of the planned calls), so a kernel's own duration can be
+read on the stream it was launched on. Import after torch (the binding does), so the name
 resolves to the runtime torch loaded.
 """
 from __future__ import annotations

@@ -56,8 +56,27 @@ class PPASError(RuntimeError):
         super().__init__(f"{what}: {status_string(status)} ({status})")
 
 
+class PlanOpts(ctypes.Structure):
+    """Planning choices of one call (0 = automatic): see ppas_plan_opts in include/ppas.h."""
+    _fields_ = [("prefill_split", ctypes.c_int32), ("decode_split", ctypes.c_int32),
+                ("tile_positions", ctypes.c_int32), ("num_cus", ctypes.c_int32)]
+
+
+class Events(ctypes.Structure):
+    """hipEvent_t handles a call's launches record (None = not recorded): see ppas_events."""
+    _fields_ = [("start", ctypes.c_void_p), ("stop", ctypes.c_void_p),
+                ("merge_start", ctypes.c_void_p), ("merge_stop", ctypes.c_void_p)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("n_items", ctypes.c_int32), ("n_merge", ctypes.c_int32), ("tile_positions", ctypes.c_int32),
+                ("n_append", ctypes.c_int32), ("workspace_bytes", ctypes.c_uint64)]
+
+
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
 _P = ctypes.POINTER(Shape)
+_O = ctypes.POINTER(PlanOpts)
+_E = ctypes.POINTER(Events)
 _lib.ppas_status_string.restype = ctypes.c_char_p
 _lib.ppas_status_string.argtypes = [ctypes.c_int]
 _lib.ppas_validate_step.restype = ctypes.c_int
@@ -71,13 +90,19 @@ _lib.ppas_attn_workspace_bytes.argtypes = [_P, _vp, _i32]
 _lib.ppas_attn_step.restype = ctypes.c_int
 _lib.ppas_attn_step.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]
 _lib.ppas_plan_items.restype = _i32
-_lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _i32, _vp, _i32]
-_lib.ppas_set_profile_events.restype = ctypes.c_int
-_lib.ppas_set_profile_events.argtypes = [_vp, _vp]
-_lib.ppas_set_split_keys.restype = ctypes.c_int
-_lib.ppas_set_split_keys.argtypes = [_i32, _i32]
-_lib.ppas_set_tile_positions.restype = ctypes.c_int
-_lib.ppas_set_tile_positions.argtypes = [_i32]
+_lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
+_lib.ppas_step_plan_create.restype = ctypes.c_int
+_lib.ppas_step_plan_create.argtypes = [_P, _vp, _i32, _vp, _i32, _O, ctypes.POINTER(ctypes.c_void_p)]
+_lib.ppas_step_plan_info.restype = ctypes.c_int
+_lib.ppas_step_plan_info.argtypes = [_vp, ctypes.POINTER(PlanInfo)]
+_lib.ppas_step_plan_destroy.restype = None
+_lib.ppas_step_plan_destroy.argtypes = [_vp]
+_lib.ppas_kv_append_planned.restype = ctypes.c_int
+_lib.ppas_kv_append_planned.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _E, _vp]
+_lib.ppas_rope_kv_append_planned.restype = ctypes.c_int
+_lib.ppas_rope_kv_append_planned.argtypes = [_vp, ctypes.c_float, _vp, _vp, _vp, _vp, _vp, _vp, _E, _vp]
+_lib.ppas_attn_step_planned.restype = ctypes.c_int
+_lib.ppas_attn_step_planned.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _E, _vp]
 
 
 def status_string(status: int) -> str:
@@ -102,8 +127,18 @@ def _host_ptr(a):
     return None if a is None else a.ctypes.data
 
 
-def _bt_host(bt_host):
-    return None if bt_host is None else np.ascontiguousarray(bt_host, dtype=np.int32)
+def _bt_host(bt_host, bt_dev=None):
+    """The host copy of the block table as int32; when the device table is given, the
+    two must have the same shape (the library reads the host copy with the device
+    table's row stride)."""
+    if bt_host is None:
+        return None
+    bt = np.ascontiguousarray(bt_host, dtype=np.int32)
+    if bt.ndim != 2:
+        raise ValueError("the host block table must be int32 [n_seqs, stride]")
+    if bt_dev is not None and tuple(bt.shape) != tuple(bt_dev.shape):
+        raise ValueError(f"host block table {tuple(bt.shape)} and device block table {tuple(bt_dev.shape)} differ")
+    return bt
 
 
 def _dev(t, name):
@@ -172,7 +207,7 @@ def validate_step(shape: Shape, desc, bt_host=None, bt_stride: int | None = None
 
 def kv_append(shape: Shape, k_pages, v_pages, k_new, v_new, desc, bt_dev, bt_host=None, stream=None) -> None:
     d = _desc(desc)
-    bt = _bt_host(bt_host)
+    bt = _bt_host(bt_host, bt_dev)
     _check_buffers(shape, d, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_kv_append(ctypes.byref(shape), _dev(k_pages, "k_pages"), _dev(v_pages, "v_pages"),
                              _dev(k_new, "k_new"), _dev(v_new, "v_new"), _host_ptr(d), len(d),
@@ -184,7 +219,7 @@ def rope_kv_append(shape: Shape, theta: float, q, k_pages, v_pages, k_new, v_new
                    stream=None) -> None:
     """Rotate q in place and k_new into the pages at each row's position; copy v_new."""
     d = _desc(desc)
-    bt = _bt_host(bt_host)
+    bt = _bt_host(bt_host, bt_dev)
     _check_buffers(shape, d, q=q, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_rope_kv_append(ctypes.byref(shape), float(theta), _dev(q, "q"), _dev(k_pages, "k_pages"),
                                   _dev(v_pages, "v_pages"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
@@ -200,7 +235,7 @@ def attn_workspace_bytes(shape: Shape, desc) -> int:
 
 def attn_step(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, workspace, bt_host=None, stream=None) -> None:
     d = _desc(desc)
-    bt = _bt_host(bt_host)
+    bt = _bt_host(bt_host, bt_dev)
     _check_buffers(shape, d, q=q, out=out, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
     st = _lib.ppas_attn_step(ctypes.byref(shape), _dev(out, "out"), _dev(q, "q"), _dev(k_pages, "k_pages"),
                              _dev(v_pages, "v_pages"), _host_ptr(d), len(d), _dev(bt_dev, "block_table"),
@@ -209,26 +244,102 @@ def attn_step(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, workspace, b
     _check(st, "ppas_attn_step")
 
 
-def plan_items(shape: Shape, desc, num_cus: int = 256) -> np.ndarray:
+def plan_opts(prefill_split: int = 0, decode_split: int = 0, tile_positions: int = 0, num_cus: int = 0) -> PlanOpts:
+    return PlanOpts(int(prefill_split), int(decode_split), int(tile_positions), int(num_cus))
+
+
+def events(start=None, stop=None, merge_start=None, merge_stop=None) -> Events:
+    return Events(start, stop, merge_start, merge_stop)
+
+
+def _opts_ptr(opts):
+    return None if opts is None else ctypes.byref(opts)
+
+
+def plan_items(shape: Shape, desc, num_cus: int = 256, opts: PlanOpts | None = None) -> np.ndarray:
     """The planned work list as int32 [n, 8]: kind, seq, kv_head, row0, pos0, npos, key_lo, key_hi."""
     d = _desc(desc)
-    n = _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), num_cus, None, 0)
+    o = PlanOpts() if opts is None else PlanOpts(opts.prefill_split, opts.decode_split, opts.tile_positions,
+                                                 opts.num_cus)
+    if o.num_cus == 0:
+        o.num_cus = int(num_cus)
+    n = _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), ctypes.byref(o), None, 0)
     if n < 0:
         raise PPASError(n, "ppas_plan_items")
     out = np.zeros((max(n, 1), 8), dtype=np.int32)
-    _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), num_cus, out.ctypes.data, n)
+    _lib.ppas_plan_items(ctypes.byref(shape), _host_ptr(d), len(d), ctypes.byref(o), out.ctypes.data, n)
     return out[:n]
 
 
-def set_split_keys(prefill: int = 0, decode: int = 0) -> None:
-    _check(_lib.ppas_set_split_keys(int(prefill), int(decode)), "ppas_set_split_keys")
+class StepPlan:
+    """A step's validated descriptors, attention work list and page-write list, made once
+    (ppas_step_plan_create) and used by any number of planned calls, e.g. one per layer."""
 
+    def __init__(self, shape: Shape, desc, bt_host=None, bt_stride: int | None = None, opts: PlanOpts | None = None):
+        self.shape = Shape(shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.page_size, shape.num_pages,
+                           shape.scale)
+        self.desc = _desc(desc)
+        bt = _bt_host(bt_host)
+        self.bt_stride = int(bt_stride if bt_stride is not None else (bt.shape[1] if bt is not None else 1))
+        if bt is not None and bt.shape[1] != self.bt_stride:
+            raise ValueError("bt_stride differs from the host block table's row length")
+        h = ctypes.c_void_p()
+        st = _lib.ppas_step_plan_create(ctypes.byref(self.shape), _host_ptr(self.desc), len(self.desc),
+                                        _host_ptr(bt), self.bt_stride, _opts_ptr(opts), ctypes.byref(h))
+        _check(st, "ppas_step_plan_create")
+        self._h = h.value
+        self.info = PlanInfo()
+        _check(_lib.ppas_step_plan_info(self._h, ctypes.byref(self.info)), "ppas_step_plan_info")
 
-def set_tile_positions(tile_positions: int = 0) -> None:
-    """Force 16- or 32-position prefill tiles (the four- or eight-wave kernel); 0 = per-step choice."""
-    _check(_lib.ppas_set_tile_positions(int(tile_positions)), "ppas_set_tile_positions")
+    @property
+    def workspace_bytes(self) -> int:
+        return int(self.info.workspace_bytes)
 
+    def _bt(self, bt_dev):
+        if bt_dev is None:
+            raise ValueError("block_table is required")
+        if bt_dev.dim() != 2 or bt_dev.shape[1] != self.bt_stride:
+            raise ValueError(f"block_table must have rows of {self.bt_stride} entries, got {tuple(bt_dev.shape)}")
+        return bt_dev
 
-def set_profile_events(start_event, stop_event) -> None:
-    """hipEvent_t handles (ints) recorded around the packed attention kernel, or (None, None)."""
-    _check(_lib.ppas_set_profile_events(start_event, stop_event), "ppas_set_profile_events")
+    def kv_append(self, k_pages, v_pages, k_new, v_new, bt_dev, events: Events | None = None, stream=None) -> None:
+        _check_buffers(self.shape, self.desc, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages,
+                       bt_dev=self._bt(bt_dev))
+        st = _lib.ppas_kv_append_planned(self._h, _dev(k_pages, "k_pages"), _dev(v_pages, "v_pages"),
+                                         _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(bt_dev, "block_table"),
+                                         None if events is None else ctypes.byref(events), _stream(stream))
+        _check(st, "ppas_kv_append_planned")
+
+    def rope_kv_append(self, theta: float, q, k_pages, v_pages, k_new, v_new, bt_dev, events: Events | None = None,
+                       stream=None) -> None:
+        _check_buffers(self.shape, self.desc, q=q, k_new=k_new, v_new=v_new, k_pages=k_pages, v_pages=v_pages,
+                       bt_dev=self._bt(bt_dev))
+        st = _lib.ppas_rope_kv_append_planned(self._h, float(theta), _dev(q, "q"), _dev(k_pages, "k_pages"),
+                                              _dev(v_pages, "v_pages"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
+                                              _dev(bt_dev, "block_table"),
+                                              None if events is None else ctypes.byref(events), _stream(stream))
+        _check(st, "ppas_rope_kv_append_planned")
+
+    def attn_step(self, out, q, k_pages, v_pages, bt_dev, workspace, events: Events | None = None,
+                  stream=None) -> None:
+        _check_buffers(self.shape, self.desc, q=q, out=out, k_pages=k_pages, v_pages=v_pages,
+                       bt_dev=self._bt(bt_dev))
+        st = _lib.ppas_attn_step_planned(self._h, _dev(out, "out"), _dev(q, "q"), _dev(k_pages, "k_pages"),
+                                         _dev(v_pages, "v_pages"), _dev(bt_dev, "block_table"),
+                                         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                         None if events is None else ctypes.byref(events), _stream(stream))
+        _check(st, "ppas_attn_step_planned")
+
+    def close(self) -> None:
+        h, self._h = getattr(self, "_h", None), None
+        if h and _lib is not None:
+            _lib.ppas_step_plan_destroy(h)
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        self.close()

@@ -63,7 +63,19 @@ class DeviceStep:
                        to_device_bf16(vh, self.device), desc, bt, bt_host, stream)
         torch.cuda.synchronize()
 
-    def append(self, stream=None, validate: bool = True) -> None:
+    def plan(self, opts=None, validate: bool = True) -> "ppas.StepPlan":
+        """A step plan for these descriptors (validated against the host block table
+        unless validate is False); the workspace grows to what the plan needs."""
+        p = ppas.StepPlan(self.shape, self.desc, self.bt_host if validate else None, self.bt_host.shape[1], opts)
+        if self.workspace.numel() < p.workspace_bytes:
+            self.workspace = torch.empty(p.workspace_bytes, dtype=torch.uint8, device=self.device)
+        return p
+
+    def append(self, stream=None, validate: bool = True, plan=None, events=None) -> None:
+        if plan is not None or events is not None:
+            p = plan or self.plan(validate=validate)
+            p.kv_append(self.k_pages, self.v_pages, self.k_new, self.v_new, self.bt, events, stream)
+            return
         ppas.kv_append(self.shape, self.k_pages, self.v_pages, self.k_new, self.v_new, self.desc, self.bt,
                        self.bt_host if validate else None, stream)
 
@@ -72,13 +84,20 @@ class DeviceStep:
         ppas.rope_kv_append(self.shape, theta, self.q, self.k_pages, self.v_pages, self.k_new, self.v_new,
                             self.desc, self.bt, self.bt_host if validate else None, stream)
 
-    def attend(self, stream=None, validate: bool = True) -> None:
+    def attend(self, stream=None, validate: bool = True, plan=None, opts=None, events=None) -> None:
+        """ppas_attn_step; with a plan, planning options or events, the planned call."""
+        if plan is not None or opts is not None or events is not None:
+            p = plan or self.plan(opts, validate)
+            if self.workspace.numel() < p.workspace_bytes:
+                self.workspace = torch.empty(p.workspace_bytes, dtype=torch.uint8, device=self.device)
+            p.attn_step(self.out, self.q, self.k_pages, self.v_pages, self.bt, self.workspace, events, stream)
+            return
         ppas.attn_step(self.shape, self.out, self.q, self.k_pages, self.v_pages, self.desc, self.bt,
                        self.workspace, self.bt_host if validate else None, stream)
 
-    def run(self, stream=None) -> None:
+    def run(self, stream=None, opts=None) -> None:
         self.append(stream)
-        self.attend(stream)
+        self.attend(stream, opts=opts)
 
     def out_f64(self) -> np.ndarray:
         return self.out.float().cpu().numpy().astype(np.float64)

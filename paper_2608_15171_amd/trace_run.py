@@ -2,10 +2,10 @@
 
 The step compositions come from the P-PAS generator (ppas_trace). Every layer
 owns its own K/V page pools; all layers share one block table (request r's
-pages are the same page ids in every layer's pools). Each step, in each layer,
-appends the step's new keys/values (ppas_kv_append) and runs the step's
-attention (ppas_attn_step); the attention kernel's own time is taken from the
-HIP events the library records around its launch.
+pages are the same page ids in every layer's pools). Each step is planned once
+(a step plan) and, in each layer, appends the step's new keys/values and runs
+the step's attention with that plan; the kernels' own times are taken from the
+HIP events their launches record.
 
 Synthetic inputs: request r's query / key / value rows at position p of layer l
 are rows base_q[r] + 97 l + p (base_kv[r] + 97 l + p) of seeded bf16 banks, so
@@ -92,7 +92,12 @@ def logical_kv_rows(setup: TraceSetup, req_id: int, layer: int, length: int):
 def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress=None):
     """Run every step of the trace in every layer. `check` lists (step index, layer)
     pairs whose outputs are copied back to the host. Returns a dict of timings and
-    the checked outputs."""
+    the checked outputs.
+
+    Each scheduler step is planned once (ppas_step_plan_create: validation, the
+    attention work list and the page-write list) and the plan serves the step's
+    page write and attention in every layer. The step's synthetic inputs for all
+    layers are gathered from the banks in one pass before its layers run."""
     import torch
     from .step import to_device_bf16
 
@@ -102,10 +107,11 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     pools = [(torch.zeros((setup.num_pages, H, D // 8, P, 8), dtype=torch.bfloat16, device=device),
               torch.zeros((setup.num_pages, H, D, P), dtype=torch.bfloat16, device=device)) for _ in range(layers)]
     ev = HipEvents()
-    attn_events, app_events = [], []
+    attn_events, app_events, gather_events = [], [], []
     checks = {}
     want = set(check)
     ws = torch.empty(256, dtype=torch.uint8, device=device)
+    shift = (LAYER_SHIFT * torch.arange(layers, device=device, dtype=torch.int64))[:, None]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -114,39 +120,41 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
         desc = st.spec.descriptors()
         rows = [setup.req_index[s.req_id] for s in st.spec.seqs]
         bt_host = np.ascontiguousarray(setup.block_table[rows])
-        bt = torch.from_numpy(bt_host).to(device, non_blocking=True)
-        need = ppas.attn_workspace_bytes(shape, desc)
-        if ws.numel() < need:
-            ws = torch.empty(need, dtype=torch.uint8, device=device)
+        bt = torch.from_numpy(bt_host).to(device)
+        plan = ppas.StepPlan(shape, desc, bt_host)
+        if ws.numel() < plan.workspace_bytes:
+            ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=device)
         T = st.spec.n_rows
         out = torch.empty((T, I.HQ, D), dtype=torch.bfloat16, device=device)
         iq0, ikv0 = step_rows(setup, st, 0)
-        iq0 = torch.from_numpy(iq0).to(device)
-        ikv0 = torch.from_numpy(ikv0).to(device)
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record()
+        iq = (torch.from_numpy(iq0).to(device)[None, :] + shift).reshape(-1)
+        ikv = (torch.from_numpy(ikv0).to(device)[None, :] + shift).reshape(-1)
+        q_all = torch.index_select(qb, 0, iq).view(layers, T, I.HQ, D)
+        k_all = torch.index_select(kb, 0, ikv).view(layers, T, H, D)
+        v_all = torch.index_select(vb, 0, ikv).view(layers, T, H, D)
+        g1.record()
+        gather_events.append((g0, g1))
         for layer in range(layers):
-            q = torch.index_select(qb, 0, iq0 + LAYER_SHIFT * layer)
-            kn = torch.index_select(kb, 0, ikv0 + LAYER_SHIFT * layer)
-            vn = torch.index_select(vb, 0, ikv0 + LAYER_SHIFT * layer)
             kp, vp = pools[layer]
-            a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a0.record()
-            ppas.kv_append(shape, kp, vp, kn, vn, desc, bt, bt_host)
-            a1.record()
+            a0, a1 = ev.create(), ev.create()
+            plan.kv_append(kp, vp, k_all[layer], v_all[layer], bt, ppas.events(a0, a1))
             app_events.append((a0, a1))
             e0, e1 = ev.create(), ev.create()
-            ppas.set_profile_events(e0, e1)
-            ppas.attn_step(shape, out, q, kp, vp, desc, bt, ws, bt_host)
-            ppas.set_profile_events(None, None)
+            plan.attn_step(out, q_all[layer], kp, vp, bt, ws, ppas.events(e0, e1))
             attn_events.append((e0, e1))
             if (si, layer) in want:
                 checks[(si, layer)] = out.float().cpu().numpy()
+        plan.close()
         if progress and si % 100 == 0:
             progress(si, len(setup.steps))
     t1.record()
     torch.cuda.synchronize()
     attn_ms = [ev.elapsed_ms(a, b) for a, b in attn_events]
-    app_ms = [a.elapsed_time(b) for a, b in app_events]
-    for a, b in attn_events:
+    app_ms = [ev.elapsed_ms(a, b) for a, b in app_events]
+    gather_ms = [a.elapsed_time(b) for a, b in gather_events]
+    for a, b in attn_events + app_events:
         ev.destroy(a)
         ev.destroy(b)
     flops = sum(M.flops(s.spec) for s in setup.steps) * layers
@@ -154,7 +162,7 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     # per scheduler iteration: attention + page writes summed over the layers
     step_ms = (np.asarray(attn_ms) + np.asarray(app_ms)).reshape(len(setup.steps), layers).sum(axis=1)
     return {"attn_ms_total": float(np.sum(attn_ms)), "kv_append_ms_total": float(np.sum(app_ms)),
-            "step_ms": step_ms,
+            "gather_ms_total": float(np.sum(gather_ms)), "step_ms": step_ms,
             "wall_ms": t0.elapsed_time(t1), "launches": len(attn_ms), "flops": flops,
             "decode_kv_bytes": dec_bytes, "attn_ms_max": float(np.max(attn_ms)), "checks": checks}
 

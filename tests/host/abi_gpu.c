@@ -59,17 +59,35 @@ static size_t k_index(int page, int g, int slot, int d) {
 }
 static size_t v_index(int page, int g, int slot, int d) { return (((size_t)page * HKV + g) * D + d) * P + slot; }
 
+/* With opts == NULL: ppas_attn_step. Otherwise a step plan made with opts, launched
+ * twice (the plan serves several calls) and destroyed. */
 static int run_step(const ppas_shape* sh, const ppas_seq* seqs, int T, void* out, void* q, void* kp, void* vp,
-                    const int32_t* bt_dev, const int32_t* bt_host, uint16_t* host_out) {
+                    const int32_t* bt_dev, const int32_t* bt_host, uint16_t* host_out, const ppas_plan_opts* opts) {
   size_t ws_bytes = ppas_attn_workspace_bytes(sh, seqs, NSEQ);
   void* ws = NULL;
-  int t, h, d;
+  int t, h, d, rep;
+  ppas_step_plan* plan = NULL;
+  ppas_plan_info info;
+  if (opts) {
+    CHECK(ppas_step_plan_create(sh, seqs, NSEQ, bt_host, STRIDE, opts, &plan) == PPAS_OK && plan != NULL);
+    CHECK(ppas_step_plan_info(plan, &info) == PPAS_OK);
+    CHECK(info.n_merge > 0);   /* the forced splits give merged rows */
+    ws_bytes = (size_t)info.workspace_bytes;
+  }
   CHECK(ws_bytes >= 256);
   HIP(hipMalloc(&ws, ws_bytes));
-  CHECK(ppas_attn_step(sh, out, q, kp, vp, seqs, NSEQ, bt_dev, STRIDE, bt_host, ws, ws_bytes - 1, NULL) ==
-        PPAS_ENOSPACE);
-  HIP(hipMemset(out, 0, (size_t)T * HQ * D * 2));
-  CHECK(ppas_attn_step(sh, out, q, kp, vp, seqs, NSEQ, bt_dev, STRIDE, bt_host, ws, ws_bytes, NULL) == PPAS_OK);
+  if (opts) {
+    CHECK(ppas_attn_step_planned(plan, out, q, kp, vp, bt_dev, ws, ws_bytes - 1, NULL, NULL) == PPAS_ENOSPACE);
+    HIP(hipMemset(out, 0, (size_t)T * HQ * D * 2));
+    for (rep = 0; rep < 2; ++rep)
+      CHECK(ppas_attn_step_planned(plan, out, q, kp, vp, bt_dev, ws, ws_bytes, NULL, NULL) == PPAS_OK);
+    ppas_step_plan_destroy(plan);
+  } else {
+    CHECK(ppas_attn_step(sh, out, q, kp, vp, seqs, NSEQ, bt_dev, STRIDE, bt_host, ws, ws_bytes - 1, NULL) ==
+          PPAS_ENOSPACE);
+    HIP(hipMemset(out, 0, (size_t)T * HQ * D * 2));
+    CHECK(ppas_attn_step(sh, out, q, kp, vp, seqs, NSEQ, bt_dev, STRIDE, bt_host, ws, ws_bytes, NULL) == PPAS_OK);
+  }
   HIP(hipDeviceSynchronize());
   HIP(hipMemcpy(host_out, out, (size_t)T * HQ * D * 2, hipMemcpyDeviceToHost));
   HIP(hipFree(ws));
@@ -153,10 +171,11 @@ int main(void) {
         }
     }
 
-  if (run_step(&sh, seqs, T, out, q, kp, vp, bt_dev, &bt[0][0], hout)) return 1;
-  CHECK(ppas_set_split_keys(64, 64) == PPAS_OK);
-  if (run_step(&sh, seqs, T, out, q, kp, vp, bt_dev, &bt[0][0], hout)) return 1;
-  CHECK(ppas_set_split_keys(0, 0) == PPAS_OK);
+  if (run_step(&sh, seqs, T, out, q, kp, vp, bt_dev, &bt[0][0], hout, NULL)) return 1;
+  {
+    ppas_plan_opts split = {64, 64, 0, 0};
+    if (run_step(&sh, seqs, T, out, q, kp, vp, bt_dev, &bt[0][0], hout, &split)) return 1;
+  }
 
   HIP(hipFree(kp));
   HIP(hipFree(vp));

@@ -164,14 +164,28 @@ void fuzz() {
     const int32_t n = int32_t(st.seqs.size());
     CHECK(validate(&sh, st.seqs.data(), n, st.bt.data(), st.stride, true) == PPAS_OK);
     const auto& sp = splits[t % 4];
-    set_split_keys(sp[0], sp[1]);
-    set_tile_positions((t / 4) % 3 == 0 ? 0 : (t / 4) % 3 == 1 ? kTilePosSmall : kTilePosLarge);
+    PlanOpts opts;
+    opts.prefill_split = sp[0];
+    opts.decode_split = sp[1];
+    opts.tile_pos = (t / 4) % 3 == 0 ? 0 : (t / 4) % 3 == 1 ? kTilePosSmall : kTilePosLarge;
     Plan plan;
-    make_plan(sh, st.seqs.data(), n, cus[t % 5], plan);
+    make_plan(sh, st.seqs.data(), n, cus[t % 5], opts, plan);
     check_plan(st, plan);
+    // the page-write list: one item per (request, touched logical page), in order
+    std::vector<AppendItem> app;
+    make_append_items(st.seqs.data(), n, app);
+    size_t k = 0;
+    for (int32_t s = 0; s < n; ++s) {
+      const ppas_seq& q = st.seqs[size_t(s)];
+      for (int32_t lp = q.cached_len / kPage; lp <= (q.cached_len + q.n_query - 1) / kPage; ++lp, ++k) {
+        CHECK(k < app.size());
+        if (k >= app.size()) break;
+        CHECK(app[k].seq == s && app[k].lpage == lp && app[k].cached_len == q.cached_len &&
+              app[k].n_query == q.n_query && app[k].query_start == q.query_start);
+      }
+    }
+    CHECK(k == app.size());
   }
-  set_split_keys(0, 0);
-  set_tile_positions(0);
 }
 
 void invalid() {
@@ -224,6 +238,23 @@ void invalid() {
     CHECK(validate(&s2, seqs.data(), 2, bt.data(), 3, true) == PPAS_EINVAL);
   }
   CHECK(validate(&sh, seqs.data(), 0, nullptr, 0, true) == PPAS_OK);   // empty step
+  {
+    // overlap checks by slot runs: one request whose logical pages 0 and 2 share a
+    // physical page clashes on slots 0..7; two requests sharing a page on disjoint
+    // slot runs (0..4 and 5..15) do not, on touching runs (0..5 and 5..15) they do
+    std::vector<ppas_seq> one = {{0, 40, 0}};
+    std::vector<int32_t> r = {5, 6, 5};
+    CHECK(validate(&sh, one.data(), 1, r.data(), 3, true) == PPAS_EINVAL);
+    CHECK(validate(&sh, one.data(), 1, r.data(), 3, false) == PPAS_OK);
+    r = {5, 6, 7};
+    CHECK(validate(&sh, one.data(), 1, r.data(), 3, true) == PPAS_OK);
+    std::vector<ppas_seq> two = {{0, 5, 16}, {5, 11, 5}};
+    std::vector<int32_t> t = {9, 9, 9, 8};   // stride 2: request 0 -> page 9 slots 0..4; request 1 -> page 9 slots 5..15
+    CHECK(validate(&sh, two.data(), 2, t.data(), 2, true) == PPAS_OK);
+    two[0].n_query = 6;
+    two[1].query_start = 6;
+    CHECK(validate(&sh, two.data(), 2, t.data(), 2, true) == PPAS_EINVAL);
+  }
 }
 
 }  // namespace

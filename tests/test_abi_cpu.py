@@ -88,6 +88,34 @@ def test_validate_block_table_range_and_overlap():
     assert ppas.validate_step(shape(), np.array([[0, 1, 21], [1, 20, 5]], np.int32), ov2) == ppas.PPAS_EINVAL
 
 
+def test_validation_cost_does_not_grow_with_the_pool():
+    """The write-overlap check follows the pages a step writes: a step of 64 requests
+    over a pool of a million pages validates about as fast as over a pool just large
+    enough for it (the check once zeroed a bitmap of the whole pool per call)."""
+    import time
+    g = I.rng(5, 1)
+    seqs = [I.Seq(1, int(c), i) for i, c in enumerate(g.integers(20000, 30000, size=60))]
+    seqs += [I.Seq(1024, 4096 * k, 60 + k) for k in range(4)]
+    spec = I.StepSpec("pool", seqs)
+    desc = spec.descriptors()
+    need = int(spec.pages_per_seq().sum())
+
+    def best(num_pages):
+        bt, _ = I.make_block_table(spec, 5, spare_pages=num_pages - need)
+        sh = shape(num_pages=num_pages)
+        assert ppas.validate_step(sh, desc, bt) == ppas.PPAS_OK
+        ts = []
+        for _ in range(30):
+            t0 = time.perf_counter()
+            ppas.validate_step(sh, desc, bt)
+            ts.append(time.perf_counter() - t0)
+        return min(ts)
+
+    small, large = best(need), best(1 << 20)
+    print(f"validate: {need} pages {small * 1e6:.1f} us, 1M pages {large * 1e6:.1f} us")
+    assert large < 2.0 * small + 20e-6
+
+
 def test_calls_reject_bad_input_before_any_device_work():
     import torch
     sh = shape()
@@ -140,13 +168,8 @@ def check_coverage(spec, items):
 @pytest.mark.parametrize("tile", [16, 32])
 def test_plan_covers_visible_keys_once(seed, splits, tile):
     spec = I.random_small_step(seed, max_seqs=6, max_n=70, max_c=300)
-    ppas.set_split_keys(*splits)
-    ppas.set_tile_positions(tile)
-    try:
-        items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256)
-    finally:
-        ppas.set_split_keys(0, 0)
-        ppas.set_tile_positions(0)
+    opts = ppas.plan_opts(splits[0], splits[1], tile)
+    items = ppas.plan_items(shape(), spec.descriptors(), num_cus=256, opts=opts)
     check_coverage(spec, items)
     assert items[items[:, 0] == 0, 5].max(initial=0) <= tile
 
@@ -163,8 +186,21 @@ def test_tile_shape_choice():
     assert npos_max(I.config_high_pressure(0)) == 16       # decode-heavy
     heavy = I.StepSpec("16k+decodes", [I.Seq(1, 25000, i) for i in range(40)] + [I.Seq(16384, 8616, 99)])
     assert npos_max(heavy) == 16
-    with pytest.raises(ppas.PPASError):
-        ppas.set_tile_positions(24)
+    for bad in (ppas.plan_opts(tile_positions=24), ppas.plan_opts(prefill_split=-1), ppas.plan_opts(decode_split=-5),
+                ppas.plan_opts(num_cus=-1)):
+        with pytest.raises(ppas.PPASError):
+            ppas.plan_items(shape(), I.config_small(0).descriptors(), opts=bad)
+
+
+def test_options_are_per_call():
+    """Planning choices travel with the call: a plan made with forced splits does not
+    change the plan of the next call without them."""
+    spec = I.config_small_budget(0)
+    base = ppas.plan_items(shape(), spec.descriptors())
+    forced = ppas.plan_items(shape(), spec.descriptors(), opts=ppas.plan_opts(64, 32, 32))
+    again = ppas.plan_items(shape(), spec.descriptors())
+    assert not np.array_equal(base, forced) and np.array_equal(base, again)
+    assert forced[forced[:, 0] == 0, 5].max() == 32
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
@@ -205,11 +241,7 @@ def test_decode_items_never_exceed_the_page_id_capacity(decode_split):
     the eight-wave one): its key range is capped at 16,384 keys, also when a larger split
     is requested."""
     spec = I.StepSpec("long-decodes", [I.Seq(1, c, i) for i, c in enumerate([0, 8191, 8192, 60000, 300000])])
-    ppas.set_split_keys(0, decode_split)
-    try:
-        items = ppas.plan_items(shape(), spec.descriptors(), num_cus=8)
-    finally:
-        ppas.set_split_keys(0, 0)
+    items = ppas.plan_items(shape(), spec.descriptors(), num_cus=8, opts=ppas.plan_opts(0, decode_split))
     dec = items[items[:, 0] == 1]
     assert (dec[:, 7] - dec[:, 6]).max() <= 16384
     assert (dec[:, 6] % 32 == 0).all(), "decode key ranges start on 32-key blocks"
@@ -235,11 +267,7 @@ def test_decode_only_steps_take_even_pieces_about_one_per_cu(num_cus):
         span = mine[:, 7] - mine[:, 6]
         assert span.max() - span.min() < 64, (s, g, span)     # boundaries on 32-key blocks
     check_coverage(spec, items)
-    ppas.set_split_keys(0, 4096)
-    try:
-        fixed = ppas.plan_items(shape(), spec.descriptors(), num_cus=num_cus)
-    finally:
-        ppas.set_split_keys(0, 0)
+    fixed = ppas.plan_items(shape(), spec.descriptors(), num_cus=num_cus, opts=ppas.plan_opts(0, 4096))
     assert ((fixed[:, 7] - fixed[:, 6]) <= 4096).all() and (fixed[:, 6] % 4096 == 0).all()
 
 

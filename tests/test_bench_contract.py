@@ -40,3 +40,21 @@ def test_json_line_fields(workload):
         assert key in roof, key
     assert roof["bound"] in ("hbm", "mfma") and 0 < roof["frac"] < 1
     assert abs(roof["frac"] - roof["achieved"] / roof["peak"]) < 1e-3
+
+
+@pytest.mark.gpu
+def test_default_line_is_the_16k_chunk_with_the_pressure_step_beside_it():
+    """With no workload flags the line is the 16,384-token chunk (where the prefill
+    target is quoted) and carries the decode-heavy pressure step as `secondary`, each
+    with its own roofline against its own bound."""
+    r = run_bench("--steps", "3", "--warmup", "3", "--no-cpu-baseline")
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip().startswith("{")]
+    assert len(lines) == 1, r.stdout
+    rec = json.loads(lines[0])
+    assert rec["config"]["workload"] == "mbt16384-chunk8616"
+    assert rec["roofline"]["bound"] == "mfma"
+    sec = rec["secondary"]
+    assert sec["config"]["workload"] == "pressure-2x1024+48dec"
+    assert sec["roofline"]["bound"] == "hbm" and 0 < sec["roofline"]["frac"] < 1
+    assert "merge_kernel_us" in sec["breakdown"] and "attn_with_merge_us" in sec["breakdown"]
