@@ -8,19 +8,21 @@ writes bit-exact. Two internal gates are stricter:
   context, where |O| ~ sqrt(e/n) ~ 0.01);
 * every element within a bound derived from the kernel's arithmetic, which is
   tight where the absolute gate is blind (rows with a few keys, |O| of order 1):
-      |gpu - O| <= 2^-8 |gpu| + (2^-9 + 6e-4) (A + |O|) + 1e-6,
+      |gpu - O| <= 2^-8 |gpu| + (2^-8 + 6e-4) (A + |O|) + 1e-6,
   with O the exact output and A the weighted mean of |V| under the same softmax
-  weights (both from the oracle). The kernel rounds each probability to bf16
-  before the PV product: a relative error of at most 2^-9 per weight, shared by
-  numerator and denominator, moves O by at most 2^-9 sum_j w_j |v_j - O| / (1 - 2^-9)
-  <= 2^-9 (1 + 2^-8) (A + |O|). The fp32 logits (128 exact bf16 products, fp32
-  sums) perturb each weight by at most ~2e-4 relative for these inputs, and the
-  fp32 accumulation of the numerator and the denominator over up to 10^4 MFMA
-  k-steps by ~1.2e-4 each; 6e-4 covers the three. The final bf16 rounding is at
-  most half an ulp, at most 2^-8 of the value. A 1-ulp gate against the rounded
-  oracle is not attainable with bf16 probabilities (two keys with weights 0.6/0.4
-  and |O| ~ 0.1 already differ by ~2 ulp), so this bound takes its place; rows
-  that see one key must equal that key's value exactly (edge-case test).
+  weights (both from the oracle). bf16 keeps 8 significant bits, so rounding to
+  nearest moves a value by at most 2^-8 of itself. The kernel rounds each
+  probability to bf16 before the PV product: a relative error of at most 2^-8 per
+  weight, shared by numerator and denominator, moves O by at most
+  2^-8 sum_j w_j |v_j - O| / (1 - 2^-8) <= 2^-8 (1 + 2^-7) (A + |O|). The fp32
+  logits (128 exact bf16 products, fp32 sums) perturb each weight by at most
+  ~2e-4 relative for these inputs, and the fp32 accumulation of the numerator and
+  the denominator over up to 10^4 MFMA k-steps by ~1.2e-4 each; 6e-4 covers the
+  three and the 2^-7 factor. The final bf16 rounding is at most 2^-8 of the value.
+  A 1-ulp gate against the rounded oracle is not attainable with bf16
+  probabilities (two keys with weights 0.6/0.4 and |O| ~ 0.1 already differ by
+  several ulp), so this bound takes its place; rows that see one key must equal
+  that key's value exactly (edge-case test).
 """
 import math
 
@@ -34,7 +36,7 @@ from paper_2608_15171_amd import inputs as I
 pytestmark = pytest.mark.gpu
 
 MAX_ABS, MEAN_ABS, ROW_REL = 1e-2, 1e-3, 1e-2
-W_REL = 2.0 ** -9 + 6e-4     # per-weight relative error budget of the derived bound
+W_REL = 2.0 ** -8 + 6e-4     # per-weight relative error budget of the derived bound
 SENTINEL = 0xFFFF      # a NaN pattern in every pool slot no request owns
 
 
