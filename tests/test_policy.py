@@ -108,11 +108,11 @@ def test_pressure_caps_prefill():
 # truth table must reject each one.
 
 MUTANTS = {
-    "strict_threshold": ("if n_p >= n_th and n_d > 0:", "if n_p > n_th and n_d > 0:"),
-    "waiting_prefills_ignored": ("n_p = n_prefill_running + n_prefill_waiting", "n_p = n_prefill_running"),
-    "decodes_ignored": ("if n_p >= n_th and n_d > 0:", "if n_p >= n_th:"),
-    "either_condition": ("if n_p >= n_th and n_d > 0:", "if n_p >= n_th or n_d > 0:"),
-    "budgets_swapped": ("        return b_cap\n    return b_max", "        return b_max\n    return b_cap"),
+    "strict_threshold": ("return prefills_pending >= n_th and", "return prefills_pending > n_th and"),
+    "waiting_prefills_ignored": ("pending = n_prefill_running + n_prefill_waiting", "pending = n_prefill_running"),
+    "decodes_ignored": ("prefills_pending >= n_th and decodes_active > 0", "prefills_pending >= n_th"),
+    "either_condition": ("prefills_pending >= n_th and decodes_active > 0", "prefills_pending >= n_th or decodes_active > 0"),
+    "budgets_swapped": ("return b_cap if under_pressure", "return b_max if under_pressure"),
 }
 
 
