@@ -18,9 +18,10 @@
  *     are ordinary host memory. The caller owns every buffer. The library
  *     allocates no device memory; it keeps a pool of pinned host buffers that
  *     hold its work lists (read by the kernels directly), released at process
- *     exit.
- *   - No state is shared between calls other than that pool: planning choices
- *     and profiling events are arguments of the calls that use them.
+ *     exit, and ppas_attn_step_noalloc uses one fixed device array per device.
+ *   - No state is shared between calls other than that pool and that array:
+ *     planning choices and profiling events are arguments of the calls that
+ *     use them.
  *   - All device work is enqueued on `hip_stream` (a hipStream_t, NULL = the
  *     null stream) and the call returns without synchronising the host. Calls
  *     on the same stream execute in order; append before attending.
@@ -62,7 +63,8 @@ typedef enum ppas_status {
   PPAS_EINVAL = -1,        /* malformed argument: null pointer, bad descriptor, bad stride */
   PPAS_ERANGE = -2,        /* a block-table entry outside [0, num_pages), a length overflow, or a step
                                too large for the int32 work list */
-  PPAS_ENOSPACE = -3,      /* workspace smaller than ppas_attn_workspace_bytes() */
+  PPAS_ENOSPACE = -3,      /* workspace smaller than ppas_attn_workspace_bytes(), or a step too large
+                               for the fixed array of ppas_attn_step_noalloc */
   PPAS_EHIP = -4,          /* a HIP runtime call or kernel launch failed */
   PPAS_EUNSUPPORTED = -5   /* shape outside the compiled set, or no gfx950 device */
 } ppas_status;
@@ -304,6 +306,38 @@ void ppas_step_plan_destroy(ppas_step_plan* plan);
  */
 int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n_seqs,
                         const ppas_plan_opts* opts, int32_t* items_out, int32_t capacity);
+
+/*
+ * For callers that cannot allocate memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc. Computes exactly what
+ * ppas_attn_step computes, with the same plan and kernels (bit-identical
+ * output), but takes no workspace and uses neither a caller buffer nor the
+ * library's pinned host pool: the step's work list (32 bytes per work item)
+ * and, after it, the fp32 partials of rows split across workgroups live in a
+ * fixed device array of PPAS_NOALLOC_SCRATCH_BYTES that every device the call
+ * runs on holds until the process ends. The call allocates nothing
+ * (no hipMalloc, hipFree, hipHostMalloc); the first call on a device looks up
+ * that device's array (hipGetSymbolAddress).
+ *
+ * The work list is copied from host memory to the array with hipMemcpyAsync on
+ * hip_stream during the call, then the attention and merge launches follow on
+ * the same stream. Every call on one device shares that device's array, which
+ * keeps the last call's contents (nothing in it needs to start at zero): calls
+ * ordered on one stream are safe, but calls that overlap in time on one device
+ * (other streams, other threads) race and give undefined results.
+ *
+ * A step whose work list and partials do not fit the array returns
+ * PPAS_ENOSPACE and enqueues nothing (steps of up to ~40 MB of partials fit,
+ * e.g. two 1,024-token chunks plus 48 decode rows of 20k-30k keys).
+ * Arguments, validation and other errors as ppas_attn_step.
+ */
+#define PPAS_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+ppas_status ppas_attn_step_noalloc(const ppas_shape* shape, void* out, const void* q,
+                                   const void* k_pages, const void* v_pages,
+                                   const ppas_seq* seqs, int32_t n_seqs,
+                                   const int32_t* block_table_dev, int32_t bt_stride,
+                                   const int32_t* block_table_host, void* hip_stream);
 
 #ifdef __cplusplus
 }

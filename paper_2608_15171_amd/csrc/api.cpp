@@ -9,17 +9,12 @@
 #include <utility>
 #include <vector>
 
+#include "device.h"
 #include "plan.h"
 #include "ppas.h"
 
 namespace ppas {
 
-hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp, const uint16_t* vp,
-                            const int32_t* bt, int32_t bt_stride, int32_t hq, int32_t hkv, float scale,
-                            const WorkItem* items, int n_items, const CombineItem* comb, int n_comb,
-                            float2* part_ml, float* part_acc, int tile_pos, hipStream_t stream,
-                            hipEvent_t ev_start, hipEvent_t ev_stop, hipEvent_t ev_merge_start,
-                            hipEvent_t ev_merge_stop);
 hipError_t launch_kv_append(uint16_t* kp, uint16_t* vp, const uint16_t* kn, const uint16_t* vn,
                             const AppendItem* items, int32_t n_items, const int32_t* bt, int32_t bt_stride,
                             int32_t hkv, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
@@ -30,14 +25,10 @@ hipError_t launch_rope_append(uint16_t* q, uint16_t* kp, uint16_t* vp, const uin
 
 namespace {
 
-struct DeviceInfo {
-  bool known = false;
-  bool gfx950 = false;
-  int cus = 256;
-};
-
 std::mutex g_dev_mu;
 std::vector<DeviceInfo> g_dev;
+
+}  // namespace
 
 // Compute-unit count and architecture of the current device (cached). Without a
 // usable device, reports 256 CUs and not-gfx950.
@@ -62,6 +53,8 @@ DeviceInfo current_device() {
   }
   return d;
 }
+
+namespace {
 
 // Work-item counts and partial-slot offsets travel as int32 (and the item count
 // sets the launch grid): a step too large for that is refused.

@@ -1,0 +1,31 @@
+// Host-side helpers shared by the entry points: kernel launchers and the
+// current device's properties.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "plan.h"
+
+namespace ppas {
+
+struct DeviceInfo {
+  bool known = false;
+  bool gfx950 = false;
+  int cus = 256;
+};
+
+// Compute-unit count and architecture of the current device (cached per device).
+// Without a usable device: 256 CUs, not gfx950.
+DeviceInfo current_device();
+
+// The packed attention launch and, when n_comb > 0, the split-merge launch.
+hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp, const uint16_t* vp,
+                            const int32_t* bt, int32_t bt_stride, int32_t hq, int32_t hkv, float scale,
+                            const WorkItem* items, int n_items, const CombineItem* comb, int n_comb,
+                            float2* part_ml, float* part_acc, int tile_pos, hipStream_t stream,
+                            hipEvent_t ev_start, hipEvent_t ev_stop, hipEvent_t ev_merge_start,
+                            hipEvent_t ev_merge_stop);
+
+}  // namespace ppas

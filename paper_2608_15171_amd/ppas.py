@@ -89,6 +89,8 @@ _lib.ppas_attn_workspace_bytes.restype = _sz
 _lib.ppas_attn_workspace_bytes.argtypes = [_P, _vp, _i32]
 _lib.ppas_attn_step.restype = ctypes.c_int
 _lib.ppas_attn_step.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]
+_lib.ppas_attn_step_noalloc.restype = ctypes.c_int
+_lib.ppas_attn_step_noalloc.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
 _lib.ppas_plan_items.restype = _i32
 _lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
 _lib.ppas_step_plan_create.restype = ctypes.c_int
@@ -242,6 +244,18 @@ def attn_step(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, workspace, b
                              bt_dev.shape[1], _host_ptr(bt), _dev(workspace, "workspace"),
                              workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "ppas_attn_step")
+
+
+def attn_step_noalloc(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, bt_host=None, stream=None) -> None:
+    """ppas_attn_step without a workspace: the library's fixed device array holds the work list
+    and the split partials (PPAS_ENOSPACE when the step does not fit it)."""
+    d = _desc(desc)
+    bt = _bt_host(bt_host, bt_dev)
+    _check_buffers(shape, d, q=q, out=out, k_pages=k_pages, v_pages=v_pages, bt_dev=bt_dev)
+    st = _lib.ppas_attn_step_noalloc(ctypes.byref(shape), _dev(out, "out"), _dev(q, "q"), _dev(k_pages, "k_pages"),
+                                     _dev(v_pages, "v_pages"), _host_ptr(d), len(d), _dev(bt_dev, "block_table"),
+                                     bt_dev.shape[1], _host_ptr(bt), _stream(stream))
+    _check(st, "ppas_attn_step_noalloc")
 
 
 def plan_opts(prefill_split: int = 0, decode_split: int = 0, tile_positions: int = 0, num_cus: int = 0) -> PlanOpts:

@@ -138,6 +138,30 @@ def test_calls_reject_bad_input_before_any_device_work():
     assert st == ppas.PPAS_EINVAL                               # no q
 
 
+def test_noalloc_refuses_oversized_steps_on_the_host():
+    """ppas_attn_step_noalloc checks the step against its fixed device array before
+    any HIP work: 1,000 decode rows of 30,001 keys plus two 1,024-token chunks need
+    ~72 MB of split partials (> PPAS_NOALLOC_SCRATCH_BYTES = 64 MiB)."""
+    d, qs = [], 0
+    for _ in range(1000):
+        d.append((qs, 1, 30000))
+        qs += 1
+    for c in (12000, 5000):
+        d.append((qs, 1024, c))
+        qs += 1024
+    desc = np.array(d, dtype=np.int32)
+    sh = shape(num_pages=10 ** 6)
+    assert ppas.attn_workspace_bytes(sh, desc) > 64 << 20
+    st = ppas._lib.ppas_attn_step_noalloc(ctypes.byref(sh), 1, 1, 1, 1, desc.ctypes.data, len(desc), 1, 1876,
+                                          None, None)
+    assert st == ppas.PPAS_ENOSPACE
+    st = ppas._lib.ppas_attn_step_noalloc(ctypes.byref(sh), None, 1, 1, 1, GOOD.ctypes.data, 2, 1, 3, None, None)
+    assert st == ppas.PPAS_EINVAL                               # no output buffer
+    bad = np.array([[0, 0, 1]], np.int32)
+    st = ppas._lib.ppas_attn_step_noalloc(ctypes.byref(sh), 1, 1, 1, 1, bad.ctypes.data, 1, 1, 3, None, None)
+    assert st == ppas.PPAS_EINVAL                               # bad descriptor
+
+
 def check_coverage(spec, items):
     """Every (row, query head) sees keys 0..p split over items without gaps or overlaps,
     and each item gives each of its rows at least one visible key."""
