@@ -246,3 +246,37 @@ def random_small_step(seed: int, max_seqs: int = 6, max_n: int = 70, max_c: int 
         else:
             seqs.append(Seq(int(g.integers(1, max_n, endpoint=True)), int(g.integers(0, max_c, endpoint=True)), i))
     return StepSpec(f"fuzz{seed}", seqs, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads)
+
+
+# ---------------------------------------------------------------------------
+# Fused gate-up projection of a decoder block's MLP (the paper's other profiled
+# prefill operation, Section 6.1). Sizes of the published Qwen2.5-3B
+# configuration: hidden 2048, intermediate 11008 (the stacked weight has 22016
+# rows). Hidden states are N(0, 1) (the scale of normalised activations);
+# weights are N(0, 0.02^2), the initialiser scale of this model family.
+GATEUP_HIDDEN, GATEUP_INTER = 2048, 11008
+GATEUP_W_STD = 0.02
+_GX, _GW = 8, 9
+_GX_BLOCK = 256   # token rows drawn per seeded block
+
+
+def gateup_weight(seed: int, hidden: int = GATEUP_HIDDEN, inter: int = GATEUP_INTER) -> np.ndarray:
+    """Stacked gate/up weight [2 * inter, hidden] as bf16 bit patterns (gate rows first)."""
+    g = rng(seed, _GW, hidden, inter)
+    return f32_to_bf16_bits(g.standard_normal(size=(2 * inter, hidden), dtype=np.float32) * np.float32(GATEUP_W_STD))
+
+
+def gateup_tokens(seed: int, n_rows: int, first_row: int = 0, hidden: int = GATEUP_HIDDEN) -> np.ndarray:
+    """Token rows first_row..first_row+n_rows-1 of a seeded prompt's hidden states [n, hidden]
+    (bf16 bits). Rows come in seeded blocks of 256, so any chunking of the prompt sees the
+    same rows as the whole prompt."""
+    out = np.empty((n_rows, hidden), dtype=np.uint16)
+    r = first_row
+    while r < first_row + n_rows:
+        b = r // _GX_BLOCK
+        blk = normal_bf16(rng(seed, _GX, hidden, b), (_GX_BLOCK, hidden))
+        lo = r - b * _GX_BLOCK
+        take = min(_GX_BLOCK - lo, first_row + n_rows - r)
+        out[r - first_row:r - first_row + take] = blk[lo:lo + take]
+        r += take
+    return out
