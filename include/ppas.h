@@ -308,6 +308,28 @@ int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n
                         const ppas_plan_opts* opts, int32_t* items_out, int32_t capacity);
 
 /*
+ * The fused gate-up projection of a decoder block's MLP, the other prefill
+ * operation the paper profiles next to attention (Section 6.1: cumulative time
+ * of eight 2k chunks against one 16k chunk, Fig. 4b; SM throughput, L2 hit rate
+ * and DRAM throughput at both chunk sizes, Table 6). The gate and up
+ * projections read the same hidden states and run as one linear layer whose
+ * weight stacks the gate rows over the up rows:
+ *   y[t][n] = sum_k x[t][k] * w[n][k]      t < n_tokens, n < n_out
+ * x [n_tokens][hidden] bf16 (the chunk's normalised hidden states), w
+ * [n_out][hidden] bf16 (row-major, gate rows 0..n_out/2-1 then up rows; any
+ * n_out >= 1 is accepted), y [n_tokens][n_out] bf16, all device memory owned by
+ * the caller. fp32 accumulation, output rounded to bf16 nearest-even; the
+ * activation that follows is not applied. One kernel launch on hip_stream
+ * (events: start/stop as for the other calls, may be NULL); no host sync.
+ * hidden must be a positive multiple of 64 (PPAS_EUNSUPPORTED otherwise);
+ * n_tokens == 0 is a no-op; NULL pointers or non-positive sizes are
+ * PPAS_EINVAL; n_tokens or n_out above 2^31 - 513, or more than 2^31 - 1
+ * output tiles of 256 x 256, is PPAS_ERANGE.
+ */
+ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden,
+                             int32_t n_out, const ppas_events* events, void* hip_stream);
+
+/*
  * For callers that cannot allocate memory: code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc. Computes exactly what
  * ppas_attn_step computes, with the same plan and kernels (bit-identical

@@ -470,6 +470,28 @@ ppas_status ppas_attn_step_planned(const ppas_step_plan* plan, void* out, const 
   }
 }
 
+ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_out,
+                             const ppas_events* events, void* hip_stream) {
+  try {
+    if (n_tokens < 0 || hidden <= 0 || n_out <= 0) return PPAS_EINVAL;
+    if (hidden % 64 != 0) return PPAS_EUNSUPPORTED;
+    const ppas_status st = check_events(events);
+    if (st != PPAS_OK) return st;
+    if (n_tokens == 0) return PPAS_OK;
+    if (!x || !w || !y) return PPAS_EINVAL;
+    // tile origins and edges stay inside int32, and the grid inside its limit
+    if (n_tokens > INT32_MAX - 512 || n_out > INT32_MAX - 512) return PPAS_ERANGE;
+    if ((int64_t(n_tokens) + 255) / 256 * ((int64_t(n_out) + 255) / 256) > INT32_MAX) return PPAS_ERANGE;
+    if (!current_device().gfx950) return PPAS_EUNSUPPORTED;
+    const hipError_t e = launch_gateup(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
+                                       static_cast<uint16_t*>(y), n_tokens, hidden, n_out,
+                                       static_cast<hipStream_t>(hip_stream), ev_of(events, 0), ev_of(events, 1));
+    return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
+  } catch (...) {
+    return PPAS_EINVAL;
+  }
+}
+
 ppas_status ppas_kv_append(const ppas_shape* shape, void* k_pages, void* v_pages, const void* k_new,
                            const void* v_new, const ppas_seq* seqs, int32_t n_seqs,
                            const int32_t* block_table_dev, int32_t bt_stride,

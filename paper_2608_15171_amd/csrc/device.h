@@ -28,4 +28,8 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
                             hipEvent_t ev_start, hipEvent_t ev_stop, hipEvent_t ev_merge_start,
                             hipEvent_t ev_merge_stop);
 
+// The gate-up projection launch: y = x w^T (hidden a multiple of 64).
+hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t T, int32_t H, int32_t N2,
+                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop);
+
 }  // namespace ppas

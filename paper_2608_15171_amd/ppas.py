@@ -91,6 +91,8 @@ _lib.ppas_attn_step.restype = ctypes.c_int
 _lib.ppas_attn_step.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp, _sz, _vp]
 _lib.ppas_attn_step_noalloc.restype = ctypes.c_int
 _lib.ppas_attn_step_noalloc.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
+_lib.ppas_gateup_proj.restype = ctypes.c_int
+_lib.ppas_gateup_proj.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _E, _vp]
 _lib.ppas_plan_items.restype = _i32
 _lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
 _lib.ppas_step_plan_create.restype = ctypes.c_int
@@ -256,6 +258,20 @@ def attn_step_noalloc(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, bt_h
                                      _dev(v_pages, "v_pages"), _host_ptr(d), len(d), _dev(bt_dev, "block_table"),
                                      bt_dev.shape[1], _host_ptr(bt), _stream(stream))
     _check(st, "ppas_attn_step_noalloc")
+
+
+def gateup_proj(x, w, y, events: Events | None = None, stream=None) -> None:
+    """y = x w^T: the fused gate-up projection (x [T, H], w [N, H], y [T, N], bf16 device tensors)."""
+    for t, name in ((x, "x"), (w, "w"), (y, "y")):
+        if t.dim() != 2 or t.element_size() != 2:
+            raise ValueError(f"{name} must be a 2-D bf16 tensor")
+    T, H = x.shape
+    N = w.shape[0]
+    if w.shape[1] != H or tuple(y.shape) != (T, N):
+        raise ValueError(f"shapes x {tuple(x.shape)}, w {tuple(w.shape)}, y {tuple(y.shape)} do not match")
+    st = _lib.ppas_gateup_proj(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N,
+                               None if events is None else ctypes.byref(events), _stream(stream))
+    _check(st, "ppas_gateup_proj")
 
 
 def plan_opts(prefill_split: int = 0, decode_split: int = 0, tile_positions: int = 0, num_cus: int = 0) -> PlanOpts:

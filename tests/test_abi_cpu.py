@@ -162,6 +162,19 @@ def test_noalloc_refuses_oversized_steps_on_the_host():
     assert st == ppas.PPAS_EINVAL                               # bad descriptor
 
 
+def test_gateup_proj_validates_before_any_device_work():
+    f = ppas._lib.ppas_gateup_proj
+    assert f(1, 1, 1, 0, 64, 8, None, None) == ppas.PPAS_OK                 # no tokens: nothing to do
+    assert f(1, 1, 1, 4, 96, 8, None, None) == ppas.PPAS_EUNSUPPORTED       # hidden not a multiple of 64
+    assert f(1, 1, 1, -1, 64, 8, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 0, 8, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 64, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(None, 1, 1, 4, 64, 8, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 2 ** 31 - 1, 64, 8, None, None) == ppas.PPAS_ERANGE
+    half = ppas.events(start=1)
+    assert f(1, 1, 1, 4, 64, 8, ctypes.byref(half), None) == ppas.PPAS_EINVAL   # start without stop
+
+
 def check_coverage(spec, items):
     """Every (row, query head) sees keys 0..p split over items without gaps or overlaps,
     and each item gives each of its rows at least one visible key."""
