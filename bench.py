@@ -40,7 +40,10 @@ WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              "rope-mbt2048": ("rope", 2), "rope-mbt16384": ("rope", 3),
              # the trace under P-PAS and under fixed 16k / 2k budgets: request latencies from
              # the measured attention time of every iteration
-             "trace-latency": None}
+             "trace-latency": None,
+             # the fused gate-up projection of the MLP (hidden 2048 -> 2 x 11008) on a chunk
+             # of 16,384 or 2,048 tokens, and one 16k prompt as 8 x 2k chunks vs 1 x 16k
+             "gateup-16384": ("gateup", 16384), "gateup-2048": ("gateup", 2048), "gateup-chunks": ("gateup", 0)}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -308,6 +311,112 @@ def run_rope_workload(args, cfg):
         err = np.abs(R.bf16_bits_to_f64(q_rot) - q_ref)
         rec["parity"] = {"rows": int(T), "max_abs": float(err.max()), "within_bound": bool((err <= tol).all()),
                          "bound": "2^-8 |exact| + 1e-6 (|x_i| + |x_(i+64)|) per element"}
+    print(json.dumps(rec), flush=True)
+
+
+def run_gateup_workload(args, T):
+    """ppas_gateup_proj, the MLP's fused gate-up projection Y = X W^T (hidden 2048, 22016
+    stacked gate/up rows: the Qwen2.5-3B sizes) on one chunk of T tokens; T = 0 runs one
+    16,384-token prompt as eight 2,048-token chunks and as one chunk (Section 6.1,
+    Fig. 4b). Weights rotate over four device copies (344 MB, more than the 256 MB
+    Infinity Cache), as a layer's weights would be evicted by the other layers' between
+    two of its launches. Kernel time from events recorded by the launch."""
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import inputs as I
+    from paper_2608_15171_amd import ppas
+    from paper_2608_15171_amd.hip_events import HipEvents
+    from paper_2608_15171_amd.step import to_device_bf16
+
+    H, N = I.GATEUP_HIDDEN, 2 * I.GATEUP_INTER
+    Tmax = 16384 if T == 0 else T
+    xb = I.gateup_tokens(args.seed, Tmax)
+    wb = I.gateup_weight(args.seed)
+    x = to_device_bf16(xb)
+    w0 = to_device_bf16(wb)
+    copies = 4
+    ws = [w0] + [w0.clone() for _ in range(copies - 1)]
+    y = torch.empty((Tmax, N), dtype=torch.bfloat16, device="cuda")
+    hip = HipEvents()
+    K = args.steps
+
+    def launch(i, rows=None, ev=None):
+        lo, n = (0, Tmax) if rows is None else rows
+        ppas.gateup_proj(x[lo:lo + n], ws[i % copies], y[lo:lo + n], ev)
+
+    def timed(chunks):
+        """Median over K rounds of the summed kernel time of the chunks (us each round)."""
+        ev = [[(hip.create(), hip.create()) for _ in chunks] for _ in range(K)]
+        for i in range(K):
+            for j, c in enumerate(chunks):
+                launch(i * len(chunks) + j, c, ppas.events(*ev[i][j]))
+        torch.cuda.synchronize()
+        per = [[hip.elapsed_ms(a, b) * 1e3 for a, b in e] for e in ev]
+        for e in ev:
+            for a, b in e:
+                hip.destroy(a)
+                hip.destroy(b)
+        return per
+
+    whole = [(0, Tmax)]
+    W = warm_up(lambda i: launch(i), args)
+    t_whole = timed(whole)
+    us = float(np.median([sum(p) for p in t_whole]))
+    F = 2.0 * Tmax * H * N
+    B = 2.0 * (Tmax * H + N * H + Tmax * N)
+    tflops = F / (us * 1e-6) / 1e12
+    wl = f"gateup-{Tmax}x{H}x{N}" if T else f"gateup-prompt16384-8x2048-vs-1x16384-{H}x{N}"
+    rec = {
+        "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(us * 1e-3, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl, "tokens": Tmax, "hidden": H, "gate_up_rows": N,
+                   "weight_copies_rotated": copies},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(f"gateup-{Tmax}", kernel="gateup_kernel"),
+                     "kernel": "gateup_kernel", "kernel_us": round(us, 2),
+                     "kernel_us_min": round(min(sum(p) for p in t_whole), 2),
+                     "per_launch": {"flop": F, "bytes": B}},
+    }
+    if T == 0:
+        chunks = [(2048 * c, 2048) for c in range(8)]
+        warm_up(lambda i: launch(i, chunks[i % 8]), args)
+        t_ch = timed(chunks)
+        per_chunk = np.median(np.array(t_ch), axis=0)
+        rec["chunks"] = {"one_16384_us": round(us, 2), "eight_2048_us": round(float(per_chunk.sum()), 2),
+                         "ratio_8x2k_over_1x16k": round(float(per_chunk.sum()) / us, 4),
+                         "per_chunk_us": [round(float(v), 2) for v in per_chunk],
+                         "paper_rtx5090_ms": {"eight_2k": 7.16, "one_16k": 6.66, "ratio": round(7.16 / 6.66, 4),
+                                              "note": "one Qwen2.5-3B decoder block on the paper's GPU; context"}}
+    if not args.no_cpu_baseline:
+        import oracle.gemm as OG
+        from threadpoolctl import threadpool_limits
+        cores = host_cores()
+        n = 16
+        with threadpool_limits(limits=cores, user_api="blas"):
+            while True:
+                rows = np.linspace(0, Tmax - 1, n).astype(np.int64)
+                t0 = time.perf_counter()
+                ref, absv = OG.gate_up(xb, wb, rows=rows, with_abs=True)
+                dt = time.perf_counter() - t0
+                if dt >= args.cpu_seconds / 4 or n >= Tmax:
+                    break
+                n = min(Tmax, n * max(2, int(args.cpu_seconds / 2 / max(dt, 1e-3))))
+        f = 2.0 * len(rows) * H * N
+        rec["cpu_baseline"] = {"value": f / dt / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+                               "sample": f"{len(rows)} of {Tmax} token rows, every output column, fp64 NumPy "
+                                         f"(operands converted in the timed call); {f:.3e} FLOP in {dt:.1f} s"}
+        # parity of the timed launch's output on the same rows
+        launch(0)
+        torch.cuda.synchronize()
+        g = y[torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
+        err = np.abs(g - ref)
+        bound = 2.0 ** -8 * np.abs(ref) + (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * absv + 1e-30
+        rec["parity"] = {"rows": int(len(rows)), "max_abs": float(err.max()), "mean_abs": float(err.mean()),
+                         "max_err_over_bound": float((err / bound).max()),
+                         "bound": "2^-8 |y| + (1 + 2^-8) 2 H 2^-24 sum_k |x_k w_k| per element"}
     print(json.dumps(rec), flush=True)
 
 
@@ -594,6 +703,8 @@ def main():
         return run_chunks_workload(args)
     if args.workload == "trace-latency":
         return run_trace_latency_workload(args)
+    if isinstance(WORKLOADS[args.workload], tuple) and WORKLOADS[args.workload][0] == "gateup":
+        return run_gateup_workload(args, WORKLOADS[args.workload][1])
     if isinstance(WORKLOADS[args.workload], tuple):
         return run_rope_workload(args, WORKLOADS[args.workload][1])
     rec = measure_step(args, args.workload, not args.no_cpu_baseline)

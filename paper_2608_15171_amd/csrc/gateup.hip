@@ -8,10 +8,16 @@
 // tile; wave (wn, wm) owns its 128 output columns x 128 token rows as 4 x 4
 // MFMA tiles (256 fp32 accumulators per lane, held in the accumulation
 // registers). The reduction advances 64 features per stage: a stage's W rows
-// and X rows (32 KB each) are copied by 16-byte global-to-LDS transfers
-// straight into MFMA operand order (operand fragment (row tile t, k-step j) at
-// (4t + j) KB, lane L at 16 L), double-buffered, so every operand read is one
-// conflict-free ds_read_b128 and each fragment feeds four MFMAs.
+// and X rows (32 KB each) are copied into LDS by 16-byte global-to-LDS
+// transfers, each covering eight whole 128-byte row runs (one cache line per
+// row), into a two-slot ring. In LDS a row keeps its eight 16-byte chunks in
+// an XOR-swizzled order, so each operand fragment read (row tile, k-step: 32
+// rows x 32 bytes) is one bank-conflict-free ds_read_b128, and each fragment
+// feeds four MFMAs. The next stage's transfers are issued a quarter per k-step
+// behind the operand reads, and the next k-step's fragments are read while the
+// current k-step's 16 MFMAs run. (Transfers of 32-byte row pieces straight into
+// operand order, and rings of four 32-feature stages, measured 33 % and 6 %
+// slower.)
 //
 // The MFMA's first operand is W (rows = output columns), its second X (rows =
 // tokens): lane L of a 32 x 32 result then holds token row L % 32 and, in
@@ -40,16 +46,29 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void global_cvoid;
 
+#ifndef PPAS_GATEUP_BK
+#define PPAS_GATEUP_BK 64
+#endif
+#ifndef PPAS_GATEUP_RING
+#define PPAS_GATEUP_RING 2
+#endif
 constexpr int kThreads = 256;
 constexpr int kBM = 256;                 // token rows per tile
 constexpr int kBN = 256;                 // output columns per tile
-constexpr int kBK = 64;                  // features per stage
-constexpr int kFrag = 1024;              // one MFMA operand fragment: 64 lanes x 16 bytes
-constexpr int kPart = 32 * kFrag;        // W (or X) rows of one stage: 8 row tiles x 4 k-steps
-constexpr int kStage = 2 * kPart;        // 64 KB
+constexpr int kBK = PPAS_GATEUP_BK;     // features per stage
+constexpr int kKSteps = kBK / 16;        // MFMA k-steps per stage
+constexpr int kRing = PPAS_GATEUP_RING;  // stages in the LDS ring; transfers run kRing - 1 stages ahead
+constexpr int kCPR = kBK / 8;            // 16-byte chunks of a row per stage
+constexpr int kRowBytes = 16 * kCPR;
+constexpr int kRowsPerDma = 64 / kCPR;   // whole rows covered by one 64-lane 16-byte transfer
+constexpr int kPart = 256 * kRowBytes;   // the 256 W (or X) rows of one stage
+constexpr int kStage = 2 * kPart;
+constexpr int kDmaPerStage = 128 / kRowsPerDma;   // transfers per wave per stage (two waves per part)
+static_assert(kBK == 32 || kBK == 64, "stages of 32 or 64 features");
+static_assert(kRing >= 2 && kRing <= 4, "a ring of two to four stages");
 constexpr int kPitch = 128 * 2 + 16;     // epilogue LDS row pitch in bytes (16-byte aligned, padded)
 constexpr int kEpiWave = 128 * kPitch;   // one wave's 128 x 128 bf16 output block
-constexpr int kSmem = (2 * kStage > 4 * kEpiWave) ? 2 * kStage : 4 * kEpiWave;
+constexpr int kSmem = (kRing * kStage > 4 * kEpiWave) ? kRing * kStage : 4 * kEpiWave;
 constexpr int kGroupM = 8;               // token-row tiles per tile-order group
 
 struct GemmArgs {
@@ -61,6 +80,13 @@ struct GemmArgs {
 };
 
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// LDS row layout of a stage: row R's 16-byte chunk c sits at position
+// c ^ swizzle(R). Sixteen consecutive rows span 256 bytes' worth of banks in
+// kRowBytes-sized rows, and the swizzle gives each of them a different position
+// for the same chunk, so the 16 lanes an operand read serves per cycle hit 16
+// different 16-byte bank groups.
+__device__ __forceinline__ int swizzle(int R) { return (R / (16 / kCPR)) % kCPR; }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
@@ -74,6 +100,19 @@ __device__ __forceinline__ void dma16(const uint16_t* g, char* lds) {
 }
 
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Workgroup barrier without a memory fence (the fence of __syncthreads would also
+// wait for the transfers still in flight for later stages). The LDS data it
+// guards is written only by the transfers, whose completion each wave waits for
+// explicitly; the empty asm keeps the compiler from moving memory accesses
+// across it.
+__device__ __forceinline__ void bare_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+}
 
 __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kSmem];
@@ -94,27 +133,32 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
   const int m0 = (first_m + in_grp % gm) * kBM;
   const int n0 = (in_grp / gm) * kBN;
 
-  // Transfers: wave w copies 16 fragments per stage: W rows (waves 0, 1) or X rows
-  // (waves 2, 3), row tiles 4(w & 1) .. 4(w & 1) + 3, k-steps 0..3 of each.
+  // Transfers: wave w copies half of one part of every stage: W rows (waves 0, 1)
+  // or X rows (waves 2, 3), rows 128(w & 1) .. 128(w & 1) + 127 of the tile. One
+  // transfer covers kRowsPerDma whole rows (the row's 16-byte chunks spread over
+  // kCPR consecutive lanes); lane L lands at 16 L, i.e. at row position L % kCPR
+  // of its row, and fetches the chunk stored there under the swizzle.
   const bool is_x = w >= 2;
-  const int rt0 = 4 * (w & 1);
-  const uint16_t* rowp[4];
+  const int half = w & 1;
+  const uint16_t* gptr[kDmaPerStage];
   {
     const uint16_t* base = is_x ? a.x : a.w;
-    const int r0 = is_x ? m0 : n0;
+    const int r0 = (is_x ? m0 : n0) + 128 * half;
     const int rmax = (is_x ? a.T : a.N2) - 1;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = min(r0 + 32 * (rt0 + q) + (lane & 31), rmax);   // rows past the edge read the last row
-      rowp[q] = base + size_t(r) * a.H + 8 * (lane >> 5);
+    for (int i = 0; i < kDmaPerStage; ++i) {
+      const int R = 128 * half + i * kRowsPerDma + lane / kCPR;      // row within the part
+      const int c = (lane % kCPR) ^ swizzle(R);
+      const int r = min(r0 + i * kRowsPerDma + lane / kCPR, rmax);   // rows past the edge read the last row
+      gptr[i] = base + size_t(r) * a.H + 8 * c;
     }
   }
-  char* const dst0 = smem + (is_x ? kPart : 0) + rt0 * 4 * kFrag;
-  auto issue = [&](int s, char* stage) {
+  const int dst0 = (is_x ? kPart : 0) + 128 * half * kRowBytes;
+  // transfers i0 .. i0 + n - 1 of stage s
+  auto issue = [&](int s, int i0, int n) {
+    char* stage = smem + (s % kRing) * kStage + dst0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) dma16(rowp[q] + s * kBK + 16 * j, stage + (dst0 - smem) + (4 * q + j) * kFrag);
+    for (int i = i0; i < i0 + n; ++i) dma16(gptr[i] + s * kBK, stage + i * kRowsPerDma * kRowBytes);
   };
 
   const int wn = w >> 1, wm = w & 1;
@@ -126,29 +170,52 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Operand fragment (row tile q, k-step j) of lane L: row 32 q + L % 32 of the
+  // wave's half, chunk 2 j + L / 32; the swizzle term depends on the lane only.
+  int roff[kKSteps];
+#pragma unroll
+  for (int j = 0; j < kKSteps; ++j)
+    roff[j] = (lane & 31) * kRowBytes + 16 * ((2 * j + (lane >> 5)) ^ swizzle(lane & 31));
+
   const int nk = a.H / kBK;
-  issue(0, smem);
-  wait_vmem();
-  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < kRing - 1; ++s)
+    if (s < nk) issue(s, 0, kDmaPerStage);
   for (int s = 0; s < nk; ++s) {
-    char* cur = smem + (s & 1) * kStage;
-    if (s + 1 < nk) issue(s + 1, smem + ((s + 1) & 1) * kStage);
-    const char* wf = cur + (4 * wn) * 4 * kFrag + 16 * lane;
-    const char* xf = cur + kPart + (4 * wm) * 4 * kFrag + 16 * lane;
+    // this wave's transfers of stage s are done once at most those of the stages
+    // after it (up to two) are still in flight; the barrier then makes every
+    // wave's part visible and tells that stage s - 1, whose ring slot the next
+    // transfers overwrite, has been read by all waves
+    const int later = min(nk - 1 - s, kRing - 2);
+    if (later >= 2)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kDmaPerStage) & 15) | (((2 * kDmaPerStage) >> 4) << 14));
+    else if (later == 1)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (kDmaPerStage & 15) | ((kDmaPerStage >> 4) << 14));
+    else
+      wait_vmem();
+    bare_barrier();
+    const bool more = s + kRing - 1 < nk;
+    const char* cur = smem + (s % kRing) * kStage;
+    const char* wf = cur + 128 * wn * kRowBytes;
+    const char* xf = cur + kPart + 128 * wm * kRowBytes;
     // The eight fragments of k-step j + 1 are read while the 16 MFMAs of k-step j
     // run (the scheduling barriers keep the reads ahead of those MFMAs).
     bf16x8 fa[2][4], fb[2][4];
     auto read = [&](int j, bf16x8 (&ra)[4], bf16x8 (&rb)[4]) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        ra[q] = as_bf16x8(lds16(wf + (4 * q + j) * kFrag));
-        rb[q] = as_bf16x8(lds16(xf + (4 * q + j) * kFrag));
+        ra[q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+        rb[q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
       }
     };
     read(0, fa[0], fb[0]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j + 1 < 4) read(j + 1, fa[(j + 1) & 1], fb[(j + 1) & 1]);
+    for (int j = 0; j < kKSteps; ++j) {
+      if (j + 1 < kKSteps) read(j + 1, fa[(j + 1) & 1], fb[(j + 1) & 1]);
+      // the next stage's transfers, a quarter per k-step, issued behind this
+      // k-step's operand reads so that the matrix cores start without waiting
+      // for the whole batch of transfers
+      if (more) issue(s + kRing - 1, j * (kDmaPerStage / kKSteps), kDmaPerStage / kKSteps);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti)
@@ -157,9 +224,8 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
           acc[ti][tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[j & 1][ti], fb[j & 1][tj], acc[ti][tj], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    wait_vmem();
-    __syncthreads();
   }
+  __syncthreads();   // every wave is done with the ring before it holds the output
 
   // Epilogue: this wave's 128 x 128 block to LDS (token-row major), then out in
   // 256-byte row runs. Result register r of MFMA tile (ti, tj): token row

@@ -13,9 +13,11 @@ a hash of the kernel's sources (for the attention kernel, with the planner's) so
 bench.py reports the traffic only while those sources are unchanged.
 
 Usage: python -m paper_2608_15171_amd.profile_summary <workload> <dir> <calib_dir> [kernel]
-       (kernel: attn_step_kernel, the default, or rope_append_kernel)
+       (kernel: attn_step_kernel, the default, rope_append_kernel or gateup_kernel)
        python -m paper_2608_15171_amd.profile_summary --mfma <workload> <dir>
-       (matrix-core utilisation from one counter pass: profiles/attn_step_kernel.<workload>.mfma.md)
+       (matrix-core utilisation from one counter pass: profiles/<kernel>.<workload>.mfma.md)
+       python -m paper_2608_15171_amd.profile_summary --cache <workload> <dir>
+       (L2 hit rate of the gate-up kernel from one counter pass: profiles/gateup_kernel.<workload>.cache.md)
 """
 from __future__ import annotations
 
@@ -30,16 +32,20 @@ SOURCES = {
     "attn_step_kernel": ["paper_2608_15171_amd/csrc/attn_step.hip", "paper_2608_15171_amd/csrc/plan.cpp",
                          "paper_2608_15171_amd/csrc/plan.h"],
     "rope_append_kernel": ["paper_2608_15171_amd/csrc/rope_append.hip"],
+    "gateup_kernel": ["paper_2608_15171_amd/csrc/gateup.hip"],
 }
 DESCRIPTION = {
     "attn_step_kernel": "One packed attention launch of the mixed step on one MI355X (gfx950); bf16 inputs, fp32 "
                         "accumulation.",
     "rope_append_kernel": "The rotary embedding of a step's new rows fused with their page write, one launch on one "
                           "MI355X (gfx950); bf16 in and out, fp32 rotation.",
+    "gateup_kernel": "The MLP's fused gate-up projection Y = X W^T (hidden 2048, 22016 stacked gate/up rows), one "
+                     "launch on one MI355X (gfx950); bf16 inputs, fp32 accumulation.",
 }
 ALGORITHMIC = {
     "attn_step_kernel": "algorithmic bytes (visible K/V once + Q + O)",
     "rope_append_kernel": "algorithmic bytes (Q read and written, new K/V read and written, once each)",
+    "gateup_kernel": "algorithmic bytes (X and W read once, Y written once)",
 }
 
 
@@ -127,10 +133,11 @@ MFMA_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_VALU
                  "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT"]
 
 
-def mfma_summary(workload: str, d: str, kernel: str = "attn_step_kernel", simds: int = 1024, xcds: int = 8):
+def mfma_summary(workload: str, d: str, kernel: str = "", simds: int = 1024, xcds: int = 8):
     """Matrix-core utilisation of the kernel from one rocprofv3 --pmc pass of MFMA_COUNTERS
     (<d>/MFMA/run_counter_collection.csv, <d>/MFMA_bench.json). SQ counters are summed over
     the chip, GRBM_GUI_ACTIVE over the XCDs; means over the pass's last two dispatches."""
+    kernel = kernel or ("gateup_kernel" if workload.startswith("gateup") else "attn_step_kernel")
     rows = list(csv.DictReader(open(os.path.join(d, "MFMA", "run_counter_collection.csv"))))
     per, dur = {}, {}
     for r in rows:
@@ -173,11 +180,12 @@ STALL_COUNTERS = ["GRBM_GUI_ACTIVE", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAI
                   "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VALU"]
 
 
-def stall_summary(workload: str, d: str, kernel: str = "attn_step_kernel", cus: int = 256, xcds: int = 8):
+def stall_summary(workload: str, d: str, kernel: str = "", cus: int = 256, xcds: int = 8):
     """Where the kernel's waves spend their time, from one rocprofv3 --pmc pass of
     STALL_COUNTERS (<d>/STALL/run_counter_collection.csv, <d>/STALL_bench.json). The SQ
     wave counters are wave-cycles in units of 4 cycles, summed over the chip; means over
     the pass's last two dispatches."""
+    kernel = kernel or ("gateup_kernel" if workload.startswith("gateup") else "attn_step_kernel")
     rows = list(csv.DictReader(open(os.path.join(d, "STALL", "run_counter_collection.csv"))))
     per, dur = {}, {}
     for r in rows:
@@ -212,10 +220,47 @@ def stall_summary(workload: str, d: str, kernel: str = "attn_step_kernel", cus: 
     print(out)
 
 
+CACHE_COUNTERS = ["GRBM_GUI_ACTIVE", "TCC_HIT_sum", "TCC_MISS_sum"]
+
+
+def cache_summary(workload: str, d: str, kernel: str = "gateup_kernel", xcds: int = 8):
+    """L2 (TCC) hit rate of the kernel from one rocprofv3 --pmc pass of CACHE_COUNTERS
+    (<d>/CACHE/run_counter_collection.csv, <d>/CACHE_bench.json), with the matrix-core
+    busy share and DRAM traffic of the other passes when present: the three quantities
+    of the paper's Table 6 (SM throughput, L2 hit rate, DRAM throughput) read on this GPU."""
+    rows = list(csv.DictReader(open(os.path.join(d, "CACHE", "run_counter_collection.csv"))))
+    per, dur = {}, {}
+    for r in rows:
+        if kernel not in r["Kernel_Name"]:
+            continue
+        c = per.setdefault(r["Dispatch_Id"], {})
+        c[r["Counter_Name"]] = c.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        dur[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    ids = sorted(per, key=int)[-2:]
+    m = {k: sum(per[i][k] for i in ids) / len(ids) for k in CACHE_COUNTERS}
+    us = sum(dur[i] for i in ids) / len(ids)
+    bench = json.loads(open(os.path.join(d, "CACHE_bench.json")).read().strip().splitlines()[-1])
+    hit = m["TCC_HIT_sum"] / max(1.0, m["TCC_HIT_sum"] + m["TCC_MISS_sum"])
+    cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(CACHE_COUNTERS)} --output-format csv -d <out> -o run "
+           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+    lines = [f"# {kernel} -- L2 hit rate, workload {bench['config']['workload']} ({workload})", "",
+             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             "| quantity | value | how it is read |", "|---|---|---|",
+             f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
+             f"| engine clock | {m['GRBM_GUI_ACTIVE'] / xcds / us / 1e3:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",
+             f"| L2 requests | {(m['TCC_HIT_sum'] + m['TCC_MISS_sum']) / 1e6:.1f} M | TCC_HIT_sum + TCC_MISS_sum |",
+             f"| L2 hit rate | {100 * hit:.1f} % | TCC_HIT_sum / (TCC_HIT_sum + TCC_MISS_sum) |", ""]
+    out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}.cache.md")
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "--mfma":
         mfma_summary(*sys.argv[2:4])
     elif sys.argv[1] == "--stalls":
         stall_summary(*sys.argv[2:4])
+    elif sys.argv[1] == "--cache":
+        cache_summary(*sys.argv[2:4])
     else:
         main(*sys.argv[1:5])
