@@ -43,7 +43,11 @@ WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              "trace-latency": None,
              # the fused gate-up projection of the MLP (hidden 2048 -> 2 x 11008) on a chunk
              # of 16,384 or 2,048 tokens, and one 16k prompt as 8 x 2k chunks vs 1 x 16k
-             "gateup-16384": ("gateup", 16384), "gateup-2048": ("gateup", 2048), "gateup-chunks": ("gateup", 0)}
+             "gateup-16384": ("gateup", 16384), "gateup-2048": ("gateup", 2048), "gateup-chunks": ("gateup", 0),
+             # request latencies of the paper's bursty trace (seconds-based, steady 0.2 req/s and
+             # swept burst rates) under P-PAS and fixed 16k / 2k budgets, every iteration's
+             # cost measured on the GPU (one full decoder layer, times 36)
+             "serving-sim": None}
 METRIC = "mixed-step attn time; prefill TFLOP/s vs MFMA peak; decode KV GB/s vs HBM"
 PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_GBPS = 8000.0     # MI355X HBM3E
@@ -341,9 +345,12 @@ def run_gateup_workload(args, T):
     hip = HipEvents()
     K = args.steps
 
+    wsb = max(ppas.gateup_workspace_bytes(Tmax, H, N), ppas.gateup_workspace_bytes(2048, H, N))
+    work = torch.empty(max(wsb, 4), dtype=torch.uint8, device="cuda") if wsb else None
+
     def launch(i, rows=None, ev=None):
         lo, n = (0, Tmax) if rows is None else rows
-        ppas.gateup_proj(x[lo:lo + n], ws[i % copies], y[lo:lo + n], ev)
+        ppas.gateup_proj(x[lo:lo + n], ws[i % copies], y[lo:lo + n], work, ev)
 
     def timed(chunks):
         """Median over K rounds of the summed kernel time of the chunks (us each round)."""
@@ -417,6 +424,96 @@ def run_gateup_workload(args, T):
         rec["parity"] = {"rows": int(len(rows)), "max_abs": float(err.max()), "mean_abs": float(err.mean()),
                          "max_err_over_bound": float((err / bound).max()),
                          "bound": "2^-8 |y| + (1 + 2^-8) 2 H 2^-24 sum_k |x_k w_k| per element"}
+    print(json.dumps(rec), flush=True)
+
+
+def run_serving_sim_workload(args):
+    """The paper's evaluation trace in seconds (Section 4.1, Fig. 2: five 10 s phases,
+    steady 0.2 requests/s alternating with a swept burst rate, Poisson arrivals;
+    25k-token prompts, 32 outputs) under P-PAS (16,384 / 2,048 by prefill pressure) and
+    fixed 16,384 and 2,048 budgets. Each iteration's duration is measured on the GPU as it
+    is scheduled: one decoder layer's kernels (QKV projection, rotary embedding + page
+    write, attention, output, gate-up and down projections) times 36 layers
+    (layer_cost.DecoderLayerCost). Reports mean and P95 end-to-end latency, TTFT and TPOT
+    per rate and rule, and the paper's geometric-mean ratios of P-PAS to each fixed rule."""
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import layer_cost as LC
+    from paper_2608_15171_amd import serving_sim as S
+
+    rates = [float(x) for x in args.burst_rates.split(",")]
+    seeds = list(range(args.seed, args.seed + args.seeds))
+    rules = {"ppas": ("ppas", 16384), "fixed16384": ("fixed", 16384), "fixed2048": ("fixed", 2048)}
+    results, parts = {}, {}
+    t_start = time.perf_counter()
+    from paper_2608_15171_amd.inputs import Seq, StepSpec
+    for rate in rates:
+        per_seed = {name: [] for name in rules}
+        parts[rate] = {}
+        for seed in seeds:
+            reqs = S.bursty_arrivals(seed, rate)
+            cost = LC.DecoderLayerCost(reqs, seed=seed)
+            # warm the clocks up on a large iteration before the timed runs
+            warm = StepSpec("warm", [Seq(16384, 0, reqs[0].req_id)])
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < args.warmup_seconds:
+                cost.layer_ms(warm)
+            cost.parts_ms = {k: 0.0 for k in cost.parts_ms}
+            for name, (mode, mbt) in rules.items():
+                res = S.simulate(reqs, cost, mode=mode, mbt=mbt)
+                per_seed[name].append(S.summarize(res))
+                print(f"serving-sim rate {rate} seed {seed} {name}: {len(res.iterations)} iterations, mean e2e "
+                      f"{per_seed[name][-1]['e2e_s']['mean']:.3f} s ({time.perf_counter() - t_start:.0f} s)",
+                      file=sys.stderr, flush=True)
+            for k, v in cost.parts_ms.items():
+                parts[rate][k] = round(parts[rate].get(k, 0.0) + v, 1)
+            cost.close()
+            del cost
+            torch.cuda.empty_cache()
+        # each statistic averaged over the seeds (the paper averages five)
+        results[rate] = {}
+        for name, runs in per_seed.items():
+            avg = {"requests": float(np.mean([r["requests"] for r in runs])),
+                   "iterations": float(np.mean([r["iterations"] for r in runs])),
+                   "makespan_s": float(np.mean([r["makespan_s"] for r in runs]))}
+            for key in ("e2e_s", "ttft_s", "tpot_s"):
+                avg[key] = {st: float(np.mean([r[key][st] for r in runs])) for st in ("mean", "p95", "max")}
+            results[rate][name] = avg
+
+    def metric(name, key, stat):
+        return [results[r][name][key][stat] for r in rates]
+
+    ratios = {}
+    for base in ("fixed16384", "fixed2048"):
+        ratios[f"ppas_vs_{base}"] = {
+            "avg_latency": round(S.geomean_ratio(metric("ppas", "e2e_s", "mean"), metric(base, "e2e_s", "mean")), 4),
+            "p95_latency": round(S.geomean_ratio(metric("ppas", "e2e_s", "p95"), metric(base, "e2e_s", "p95")), 4),
+            "avg_ttft": round(S.geomean_ratio(metric("ppas", "ttft_s", "mean"), metric(base, "ttft_s", "mean")), 4),
+            "avg_tpot": round(S.geomean_ratio(metric("ppas", "tpot_s", "mean"), metric(base, "tpot_s", "mean")), 4)}
+    e16, e2 = metric("fixed16384", "e2e_s", "mean"), metric("fixed2048", "e2e_s", "mean")
+    better = ["16k" if a < b else "2k" for a, b in zip(e16, e2)]
+    ppas_mean = metric("ppas", "e2e_s", "mean")
+    rec = {
+        "metric": "serving simulation: mean end-to-end request latency under P-PAS (geometric mean over burst rates)",
+        "value": round(float(np.exp(np.mean(np.log(ppas_mean)))), 4), "unit": "s", "n_gpus": 1,
+        "steps": len(rates), "warmup": 0, "ms_per_step": None, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "serving-sim-bursty-50s", "phases_s": [10] * 5, "steady_rate": 0.2,
+                   "burst_rates": rates, "prompt_tokens": 25000, "output_tokens": 32, "layers": 36,
+                   "model_shape": "Qwen2.5-3B (hidden 2048, intermediate 11008, 16q/2kv heads, head_dim 128)",
+                   "iteration_cost": "one decoder layer measured per iteration x 36: QKV, rope+page write, "
+                                     "attention (+merge), o, gate-up, down; norms, SiLU-mul, residuals, "
+                                     "LM head not included", "seeds": seeds},
+        "results": {str(r): {k: {m: (None if v[m] is None else {s: round(x, 4) for s, x in v[m].items()})
+                                 if isinstance(v[m], dict) or v[m] is None else v[m]
+                                 for m in v} for k, v in results[r].items()} for r in rates},
+        "lower_latency_fixed_rule_per_rate": dict(zip([str(r) for r in rates], better)),
+        "crossover": better[0] == "16k" and "2k" in better,
+        "ratios": ratios,
+        "kernel_ms_per_layer_summed": {str(r): parts[r] for r in rates},
+        "wall_s": round(time.perf_counter() - t_start, 1),
+    }
     print(json.dumps(rec), flush=True)
 
 
@@ -686,6 +783,9 @@ def main():
     ap.add_argument("--prompt", type=int, default=16384, help="chunks workload: prompt tokens")
     ap.add_argument("--chunk", type=int, default=2048, help="chunks workload: tokens per chunk")
     ap.add_argument("--rope-theta", type=float, default=1e6, help="rope workloads: rotary base")
+    ap.add_argument("--burst-rates", default="1,2,3,4,5",
+                    help="serving-sim workload: burst-phase arrival rates (requests/s)")
+    ap.add_argument("--seeds", type=int, default=3, help="serving-sim workload: traces per rate (seeds 0..n-1)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "
@@ -703,6 +803,8 @@ def main():
         return run_chunks_workload(args)
     if args.workload == "trace-latency":
         return run_trace_latency_workload(args)
+    if args.workload == "serving-sim":
+        return run_serving_sim_workload(args)
     if isinstance(WORKLOADS[args.workload], tuple) and WORKLOADS[args.workload][0] == "gateup":
         return run_gateup_workload(args, WORKLOADS[args.workload][1])
     if isinstance(WORKLOADS[args.workload], tuple):

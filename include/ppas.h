@@ -319,15 +319,29 @@ int32_t ppas_plan_items(const ppas_shape* shape, const ppas_seq* seqs, int32_t n
  * [n_out][hidden] bf16 (row-major, gate rows 0..n_out/2-1 then up rows; any
  * n_out >= 1 is accepted), y [n_tokens][n_out] bf16, all device memory owned by
  * the caller. fp32 accumulation, output rounded to bf16 nearest-even; the
- * activation that follows is not applied. One kernel launch on hip_stream
- * (events: start/stop as for the other calls, may be NULL); no host sync.
+ * activation that follows is not applied. When a call's 256 x 256 output
+ * tiles are fewer than the device's compute units, the reduction over hidden
+ * is split across several workgroups per tile; their fp32 partial sums go to
+ * the caller's workspace (ppas_gateup_workspace_bytes, device memory, not read
+ * before written, not shared with a call still in flight) and a second launch
+ * adds them in a fixed order. A workspace smaller than that (NULL with 0 bytes
+ * included) gives fewer splits, down to none: results are deterministic for a
+ * given shape and workspace size, and every split count stays within the same
+ * rounding bound. The kernels run on hip_stream (events: start on the first
+ * launch, stop on the last, as for the other calls; may be NULL); no host sync.
  * hidden must be a positive multiple of 64 (PPAS_EUNSUPPORTED otherwise);
- * n_tokens == 0 is a no-op; NULL pointers or non-positive sizes are
- * PPAS_EINVAL; n_tokens or n_out above 2^31 - 513, or more than 2^31 - 1
- * output tiles of 256 x 256, is PPAS_ERANGE.
+ * n_tokens == 0 is a no-op; NULL pointers (a NULL workspace with a non-zero
+ * size included) or non-positive sizes are PPAS_EINVAL; n_tokens or n_out above
+ * 2^31 - 513, or more than 2^31 - 1 output tiles of 256 x 256, is PPAS_ERANGE.
  */
 ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden,
-                             int32_t n_out, const ppas_events* events, void* hip_stream);
+                             int32_t n_out, void* workspace, size_t workspace_bytes,
+                             const ppas_events* events, void* hip_stream);
+
+/* Workspace ppas_gateup_proj uses for this shape on the current device (0 when
+ * it does not split the reduction, or for an invalid shape). The library's own
+ * sizing call: the paper describes no workspace. */
+size_t ppas_gateup_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_out);
 
 /*
  * For callers that cannot allocate memory: code under HIP graph capture, tight

@@ -470,22 +470,47 @@ ppas_status ppas_attn_step_planned(const ppas_step_plan* plan, void* out, const 
   }
 }
 
-ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_out,
-                             const ppas_events* events, void* hip_stream) {
+namespace {
+
+ppas_status check_gateup(int32_t n_tokens, int32_t hidden, int32_t n_out) {
+  if (n_tokens < 0 || hidden <= 0 || n_out <= 0) return PPAS_EINVAL;
+  if (hidden % 64 != 0) return PPAS_EUNSUPPORTED;
+  // tile origins and edges stay inside int32, and the grid inside its limit
+  if (n_tokens > INT32_MAX - 512 || n_out > INT32_MAX - 512) return PPAS_ERANGE;
+  if (gateup_tiles(n_tokens, n_out) > INT32_MAX) return PPAS_ERANGE;
+  return PPAS_OK;
+}
+
+}  // namespace
+
+size_t ppas_gateup_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_out) {
   try {
-    if (n_tokens < 0 || hidden <= 0 || n_out <= 0) return PPAS_EINVAL;
-    if (hidden % 64 != 0) return PPAS_EUNSUPPORTED;
-    const ppas_status st = check_events(events);
+    if (check_gateup(n_tokens, hidden, n_out) != PPAS_OK || n_tokens == 0) return 0;
+    return gateup_workspace_bytes(n_tokens, n_out, gateup_splits(n_tokens, hidden, n_out, current_device().cus));
+  } catch (...) {
+    return 0;
+  }
+}
+
+ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_out,
+                             void* workspace, size_t workspace_bytes, const ppas_events* events, void* hip_stream) {
+  try {
+    ppas_status st = check_gateup(n_tokens, hidden, n_out);
+    if (st != PPAS_OK) return st;
+    st = check_events(events);
     if (st != PPAS_OK) return st;
     if (n_tokens == 0) return PPAS_OK;
-    if (!x || !w || !y) return PPAS_EINVAL;
-    // tile origins and edges stay inside int32, and the grid inside its limit
-    if (n_tokens > INT32_MAX - 512 || n_out > INT32_MAX - 512) return PPAS_ERANGE;
-    if ((int64_t(n_tokens) + 255) / 256 * ((int64_t(n_out) + 255) / 256) > INT32_MAX) return PPAS_ERANGE;
-    if (!current_device().gfx950) return PPAS_EUNSUPPORTED;
+    if (!x || !w || !y || (workspace_bytes > 0 && !workspace)) return PPAS_EINVAL;
+    const DeviceInfo dev = current_device();
+    if (!dev.gfx950) return PPAS_EUNSUPPORTED;
+    // the automatic split, reduced to what the workspace holds (no split needs none)
+    int splits = gateup_splits(n_tokens, hidden, n_out, dev.cus);
+    while (splits > 1 && gateup_workspace_bytes(n_tokens, n_out, splits) > workspace_bytes) --splits;
+    if (gateup_tiles(n_tokens, n_out) * splits > INT32_MAX) splits = 1;
     const hipError_t e = launch_gateup(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
-                                       static_cast<uint16_t*>(y), n_tokens, hidden, n_out,
-                                       static_cast<hipStream_t>(hip_stream), ev_of(events, 0), ev_of(events, 1));
+                                       static_cast<uint16_t*>(y), n_tokens, hidden, n_out, splits,
+                                       static_cast<float*>(workspace), static_cast<hipStream_t>(hip_stream),
+                                       ev_of(events, 0), ev_of(events, 1));
     return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
   } catch (...) {
     return PPAS_EINVAL;

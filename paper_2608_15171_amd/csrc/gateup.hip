@@ -32,6 +32,9 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <type_traits>
+#include <cstddef>
 #include <cstdint>
 
 namespace ppas {
@@ -41,6 +44,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
@@ -54,6 +58,7 @@ typedef __attribute__((address_space(1))) const void global_cvoid;
 #endif
 constexpr int kThreads = 256;
 constexpr int kBM = 256;                 // token rows per tile
+constexpr int kBMTail = 64;              // token rows per tile of the last T % 256 rows
 constexpr int kBN = 256;                 // output columns per tile
 constexpr int kBK = PPAS_GATEUP_BK;     // features per stage
 constexpr int kKSteps = kBK / 16;        // MFMA k-steps per stage
@@ -75,8 +80,11 @@ struct GemmArgs {
   const uint16_t* x;
   const uint16_t* w;
   uint16_t* y;
+  float* part;            // splits > 1: fp32 partial sums [splits][T][N2]
   int32_t T, H, N2;
-  int32_t tiles_m, tiles_n;
+  int32_t tiles_m, tiles_n;   // full 256-row tiles, 256-column tiles
+  int32_t tail_m;             // 64-row tiles of the last T % 256 rows
+  int32_t splits;             // reduction split over this many workgroups per tile
 };
 
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
@@ -114,99 +122,118 @@ __device__ __forceinline__ void bare_barrier() {
   asm volatile("" ::: "memory");
 }
 
-__global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem[kSmem];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-
-  // blockIdx -> tile: the first 8 * (tiles / 8) workgroups give XCD b % 8 the
-  // contiguous range of tiles xcd * (tiles / 8) + ...; the remainder runs in order.
-  const int ntiles = a.tiles_m * a.tiles_n;
-  const int per_xcd = ntiles / 8;
-  const int b = blockIdx.x;
-  const int t = (b < 8 * per_xcd) ? (b % 8) * per_xcd + b / 8 : b;
-  const int grp = t / (kGroupM * a.tiles_n);
-  const int first_m = grp * kGroupM;
-  const int gm = min(kGroupM, a.tiles_m - first_m);
-  const int in_grp = t - grp * kGroupM * a.tiles_n;
-  const int m0 = (first_m + in_grp % gm) * kBM;
-  const int n0 = (in_grp / gm) * kBN;
+// One output tile of BM token rows x 256 columns over stages k_lo .. k_hi - 1.
+// BM = 256 (full tiles) or 64 (the ragged last rows of the tokens, and calls of
+// fewer than 256 tokens): wave (wn, wm) owns 128 columns x BM / 2 rows, i.e.
+// 4 x BM / 64 MFMA tiles. The W part of a stage is always 256 rows (waves 0 and
+// 1 copy 128 each), the X part BM rows (waves 2 and 3 copy BM / 2 each).
+template <int BM>
+__device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0, int n0, int split, int k_lo,
+                                          int k_hi) {
+  constexpr int kMT = BM / 64;                       // MFMA row tiles of a wave in the token dimension
+  constexpr int kDmaX = (BM / 2) / kRowsPerDma;      // transfers per X wave per stage
+  constexpr int kDmaMax = kDmaPerStage;              // a W wave's count (the larger)
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
   // Transfers: wave w copies half of one part of every stage: W rows (waves 0, 1)
-  // or X rows (waves 2, 3), rows 128(w & 1) .. 128(w & 1) + 127 of the tile. One
-  // transfer covers kRowsPerDma whole rows (the row's 16-byte chunks spread over
-  // kCPR consecutive lanes); lane L lands at 16 L, i.e. at row position L % kCPR
-  // of its row, and fetches the chunk stored there under the swizzle.
+  // or X rows (waves 2, 3). One transfer covers kRowsPerDma whole rows (the row's
+  // 16-byte chunks spread over kCPR consecutive lanes); lane L lands at 16 L, i.e.
+  // at row position L % kCPR of its row, and fetches the chunk stored there under
+  // the swizzle.
   const bool is_x = w >= 2;
   const int half = w & 1;
-  const uint16_t* gptr[kDmaPerStage];
+  const int rows_half = is_x ? BM / 2 : 128;
+  const int ndma = is_x ? kDmaX : kDmaMax;
+  const uint16_t* gptr[kDmaMax];
   {
     const uint16_t* base = is_x ? a.x : a.w;
-    const int r0 = (is_x ? m0 : n0) + 128 * half;
+    const int r0 = (is_x ? m0 : n0) + rows_half * half;
     const int rmax = (is_x ? a.T : a.N2) - 1;
 #pragma unroll
-    for (int i = 0; i < kDmaPerStage; ++i) {
-      const int R = 128 * half + i * kRowsPerDma + lane / kCPR;      // row within the part
+    for (int i = 0; i < kDmaMax; ++i) {
+      const int R = rows_half * half + i * kRowsPerDma + lane / kCPR;   // row within the part
       const int c = (lane % kCPR) ^ swizzle(R);
-      const int r = min(r0 + i * kRowsPerDma + lane / kCPR, rmax);   // rows past the edge read the last row
+      const int r = min(r0 + i * kRowsPerDma + lane / kCPR, rmax);     // rows past the edge read the last row
       gptr[i] = base + size_t(r) * a.H + 8 * c;
     }
   }
-  const int dst0 = (is_x ? kPart : 0) + 128 * half * kRowBytes;
-  // transfers i0 .. i0 + n - 1 of stage s
-  auto issue = [&](int s, int i0, int n) {
+  const int dst0 = (is_x ? kPart : 0) + rows_half * half * kRowBytes;
+  // this wave's transfers i0 .. i0 + n - 1 of stage s (n a compile-time count)
+  auto issue = [&](int s, int i0, auto n) {
     char* stage = smem + (s % kRing) * kStage + dst0;
 #pragma unroll
-    for (int i = i0; i < i0 + n; ++i) dma16(gptr[i] + s * kBK, stage + i * kRowsPerDma * kRowBytes);
+    for (int i = 0; i < decltype(n)::value; ++i)
+      dma16(gptr[i0 + i] + s * kBK, stage + (i0 + i) * kRowsPerDma * kRowBytes);
   };
+  auto issue_all = [&](int s) {
+    if (is_x)
+      issue(s, 0, std::integral_constant<int, kDmaX>{});
+    else
+      issue(s, 0, std::integral_constant<int, kDmaMax>{});
+  };
+  // a quarter of the stage's transfers per k-step
+  auto issue_part = [&](int s, int j) {
+    if (is_x)
+      issue(s, j * (kDmaX / kKSteps), std::integral_constant<int, kDmaX / kKSteps>{});
+    else
+      issue(s, j * (kDmaMax / kKSteps), std::integral_constant<int, kDmaMax / kKSteps>{});
+  };
+  static_assert(kDmaX % kKSteps == 0 && kDmaMax % kKSteps == 0, "transfers split evenly over the k-steps");
+  (void)ndma;
 
   const int wn = w >> 1, wm = w & 1;
-  f32x16 acc[4][4];
+  f32x16 acc[4][kMT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < kMT; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // Operand fragment (row tile q, k-step j) of lane L: row 32 q + L % 32 of the
-  // wave's half, chunk 2 j + L / 32; the swizzle term depends on the lane only.
+  // wave's rows, chunk 2 j + L / 32; the swizzle term depends on the lane only.
   int roff[kKSteps];
 #pragma unroll
   for (int j = 0; j < kKSteps; ++j)
     roff[j] = (lane & 31) * kRowBytes + 16 * ((2 * j + (lane >> 5)) ^ swizzle(lane & 31));
 
-  const int nk = a.H / kBK;
 #pragma unroll
   for (int s = 0; s < kRing - 1; ++s)
-    if (s < nk) issue(s, 0, kDmaPerStage);
-  for (int s = 0; s < nk; ++s) {
+    if (k_lo + s < k_hi) issue_all(k_lo + s);
+  for (int s = k_lo; s < k_hi; ++s) {
     // this wave's transfers of stage s are done once at most those of the stages
     // after it (up to two) are still in flight; the barrier then makes every
     // wave's part visible and tells that stage s - 1, whose ring slot the next
     // transfers overwrite, has been read by all waves
-    const int later = min(nk - 1 - s, kRing - 2);
-    if (later >= 2)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kDmaPerStage) & 15) | (((2 * kDmaPerStage) >> 4) << 14));
-    else if (later == 1)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | (kDmaPerStage & 15) | ((kDmaPerStage >> 4) << 14));
-    else
+    const int later = min(k_hi - 1 - s, kRing - 2);
+    const int per = is_x ? kDmaX : kDmaMax;
+    if (later >= 2) {
+      if (per == 16)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | ((32) & 15) | (((32) >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kDmaX) & 15) | (((2 * kDmaX) >> 4) << 14));
+    } else if (later == 1) {
+      if (per == 16)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | (16 & 15) | ((16 >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0x0F70 | (kDmaX & 15) | ((kDmaX >> 4) << 14));
+    } else {
       wait_vmem();
+    }
     bare_barrier();
-    const bool more = s + kRing - 1 < nk;
+    const bool more = s + kRing - 1 < k_hi;
     const char* cur = smem + (s % kRing) * kStage;
     const char* wf = cur + 128 * wn * kRowBytes;
-    const char* xf = cur + kPart + 128 * wm * kRowBytes;
-    // The eight fragments of k-step j + 1 are read while the 16 MFMAs of k-step j
-    // run (the scheduling barriers keep the reads ahead of those MFMAs).
-    bf16x8 fa[2][4], fb[2][4];
-    auto read = [&](int j, bf16x8 (&ra)[4], bf16x8 (&rb)[4]) {
+    const char* xf = cur + kPart + (BM / 2) * wm * kRowBytes;
+    // The fragments of k-step j + 1 are read while the MFMAs of k-step j run (the
+    // scheduling barriers keep the reads ahead of those MFMAs).
+    bf16x8 fa[2][4], fb[2][kMT];
+    auto read = [&](int j, bf16x8 (&ra)[4], bf16x8 (&rb)[kMT]) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        ra[q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
-        rb[q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
-      }
+      for (int q = 0; q < 4; ++q) ra[q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+#pragma unroll
+      for (int q = 0; q < kMT; ++q) rb[q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
     };
     read(0, fa[0], fb[0]);
 #pragma unroll
@@ -215,26 +242,54 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
       // the next stage's transfers, a quarter per k-step, issued behind this
       // k-step's operand reads so that the matrix cores start without waiting
       // for the whole batch of transfers
-      if (more) issue(s + kRing - 1, j * (kDmaPerStage / kKSteps), kDmaPerStage / kKSteps);
+      if (more) issue_part(s + kRing - 1, j);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti)
 #pragma unroll
-        for (int tj = 0; tj < 4; ++tj)
+        for (int tj = 0; tj < kMT; ++tj)
           acc[ti][tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[j & 1][ti], fb[j & 1][tj], acc[ti][tj], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
   __syncthreads();   // every wave is done with the ring before it holds the output
 
-  // Epilogue: this wave's 128 x 128 block to LDS (token-row major), then out in
-  // 256-byte row runs. Result register r of MFMA tile (ti, tj): token row
-  // 32 tj + L % 32, column 32 ti + 8(r / 4) + 4(L / 32) + r % 4.
+  // Result register r of MFMA tile (ti, tj): token row 32 tj + L % 32 of the
+  // wave's rows, column 32 ti + 8(r / 4) + 4(L / 32) + r % 4 of its columns.
+  const int mw = m0 + (BM / 2) * wm, nw = n0 + 128 * wn;
+  if (a.splits > 1) {
+    // fp32 partial sums of this split, straight from the accumulators: four
+    // consecutive columns of one token row per (ti, tj, g)
+    float* pb = a.part + size_t(split) * a.T * a.N2;
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+      for (int tj = 0; tj < kMT; ++tj) {
+        const int m = mw + 32 * tj + (lane & 31);
+        if (m >= a.T) continue;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nw + 32 * ti + 8 * g + 4 * (lane >> 5);
+          float* dst = pb + size_t(m) * a.N2 + n;
+          if (n + 4 <= a.N2 && (a.N2 & 3) == 0) {
+            *reinterpret_cast<f32x4*>(dst) =
+                f32x4{acc[ti][tj][4 * g], acc[ti][tj][4 * g + 1], acc[ti][tj][4 * g + 2], acc[ti][tj][4 * g + 3]};
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (n + e < a.N2) dst[e] = acc[ti][tj][4 * g + e];
+          }
+        }
+      }
+    return;
+  }
+
+  // bf16: the wave's block to LDS (token-row major), then out in 256-byte row runs.
   char* eb = smem + w * kEpiWave;
 #pragma unroll
   for (int ti = 0; ti < 4; ++ti)
 #pragma unroll
-    for (int tj = 0; tj < 4; ++tj)
+    for (int tj = 0; tj < kMT; ++tj)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int row = 32 * tj + (lane & 31);
@@ -245,11 +300,11 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
         *reinterpret_cast<u32x2*>(eb + row * kPitch + col * 2) = v;
       }
   __syncthreads();
-  const int mb = m0 + 128 * wm, nb = n0 + 128 * wn + 8 * (lane & 15);
+  const int nb = nw + 8 * (lane & 15);
 #pragma unroll 4
-  for (int s = 0; s < 32; ++s) {
+  for (int s = 0; s < BM / 8; ++s) {
     const int row = 4 * s + (lane >> 4);
-    const int m = mb + row;
+    const int m = mw + row;
     if (m >= a.T) break;
     const u32x4 v = lds16(eb + row * kPitch + 16 * (lane & 15));
     uint16_t* dst = a.y + size_t(m) * a.N2 + nb;
@@ -263,23 +318,105 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
   }
 }
 
+__global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem[kSmem];
+
+  // blockIdx -> (tile, split): the first 8 * (items / 8) workgroups give XCD b % 8
+  // the contiguous range of items xcd * (items / 8) + ...; the remainder runs in
+  // order. Item u is tile u % tiles of reduction split u / tiles, so the
+  // workgroups next to each other on an XCD work on neighbouring tiles of the
+  // same split. Tiles 0 .. full - 1 are the 256-row tiles (in groups of 8 that
+  // share a weight tile), the rest the 64-row tiles of the last T % 256 rows.
+  const int full = a.tiles_m * a.tiles_n;
+  const int ntiles = full + a.tail_m * a.tiles_n;
+  const int nitems = ntiles * a.splits;
+  const int per_xcd = nitems / 8;
+  const int b = blockIdx.x;
+  const int u = (b < 8 * per_xcd) ? (b % 8) * per_xcd + b / 8 : b;
+  const int t = u % ntiles;
+  const int split = u / ntiles;
+  const int nk_all = a.H / kBK;
+  const int k_lo = int(int64_t(split) * nk_all / a.splits);
+  const int k_hi = int(int64_t(split + 1) * nk_all / a.splits);
+  if (t < full) {
+    const int grp = t / (kGroupM * a.tiles_n);
+    const int first_m = grp * kGroupM;
+    const int gm = min(kGroupM, a.tiles_m - first_m);
+    const int in_grp = t - grp * kGroupM * a.tiles_n;
+    tile_body<kBM>(a, smem, (first_m + in_grp % gm) * kBM, (in_grp / gm) * kBN, split, k_lo, k_hi);
+  } else {
+    const int tt = t - full;
+    tile_body<kBMTail>(a, smem, a.tiles_m * kBM + (tt % a.tail_m) * kBMTail, (tt / a.tail_m) * kBN, split, k_lo,
+                       k_hi);
+  }
+}
+
+// y = bf16(sum over splits of the partials), the splits summed in order; thread i
+// covers elements 4i .. 4i + 3 of the flattened [T][N2] output.
+__global__ __launch_bounds__(256) void gateup_reduce_kernel(const float* part, uint16_t* y, int64_t total,
+                                                            int32_t splits) {
+  const int64_t e0 = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (e0 >= total) return;
+  if (e0 + 4 <= total) {
+    f32x4 s = *reinterpret_cast<const f32x4*>(part + e0);
+    for (int k = 1; k < splits; ++k) s += *reinterpret_cast<const f32x4*>(part + size_t(k) * total + e0);
+    u32x2 v;
+    v[0] = pack_bf16x2(s[0], s[1]);
+    v[1] = pack_bf16x2(s[2], s[3]);
+    *reinterpret_cast<u32x2*>(y + e0) = v;
+  } else {
+    for (int64_t e = e0; e < total; ++e) {
+      float s = part[e];
+      for (int k = 1; k < splits; ++k) s += part[size_t(k) * total + e];
+      y[e] = uint16_t(pack_bf16x2(s, 0.f) & 0xffff);
+    }
+  }
+}
+
 }  // namespace
 
+int64_t gateup_tiles(int32_t T, int32_t N2) {
+  return (int64_t(T / kBM) + (T % kBM + kBMTail - 1) / kBMTail) * ((N2 + kBN - 1) / kBN);
+}
+
+int gateup_splits(int32_t T, int32_t H, int32_t N2, int cus) {
+  const int64_t tiles = gateup_tiles(T, N2);
+  const int nk = H / kBK;
+  if (tiles <= 0 || tiles >= cus) return 1;
+  // about one workgroup per compute unit, each with at least four stages
+  return int(std::max<int64_t>(1, std::min<int64_t>(cus / tiles, nk / 4)));
+}
+
+size_t gateup_workspace_bytes(int32_t T, int32_t N2, int splits) {
+  return splits > 1 ? size_t(splits) * size_t(T) * size_t(N2) * sizeof(float) : 0;
+}
+
 hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t T, int32_t H, int32_t N2,
-                         hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                         int splits, float* part, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
   GemmArgs a;
   a.x = x;
   a.w = w;
   a.y = y;
+  a.part = part;
   a.T = T;
   a.H = H;
   a.N2 = N2;
-  a.tiles_m = (T + kBM - 1) / kBM;
+  a.tiles_m = T / kBM;
+  a.tail_m = (T % kBM + kBMTail - 1) / kBMTail;
   a.tiles_n = (N2 + kBN - 1) / kBN;
-  const int64_t n = int64_t(a.tiles_m) * a.tiles_n;
+  a.splits = splits;
+  const int64_t n = gateup_tiles(T, N2) * splits;
   if (n <= 0) return hipSuccess;
-  if (n > INT32_MAX) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL(gateup_kernel, dim3(unsigned(n)), dim3(kThreads), 0, stream, ev_start, ev_stop, 0, a);
+  if (n > INT32_MAX || splits < 1 || splits > H / kBK || (splits > 1 && !part)) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(gateup_kernel, dim3(unsigned(n)), dim3(kThreads), 0, stream, ev_start,
+                        splits > 1 ? nullptr : ev_stop, 0, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t total = int64_t(T) * N2;
+  const int64_t blocks = (total + 1023) / 1024;
+  if (blocks > INT32_MAX) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(gateup_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, nullptr, ev_stop, 0,
+                        static_cast<const float*>(part), y, total, splits);
   return hipGetLastError();
 }
 

@@ -92,7 +92,9 @@ _lib.ppas_attn_step.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _v
 _lib.ppas_attn_step_noalloc.restype = ctypes.c_int
 _lib.ppas_attn_step_noalloc.argtypes = [_P, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]
 _lib.ppas_gateup_proj.restype = ctypes.c_int
-_lib.ppas_gateup_proj.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _E, _vp]
+_lib.ppas_gateup_proj.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _sz, _E, _vp]
+_lib.ppas_gateup_workspace_bytes.restype = _sz
+_lib.ppas_gateup_workspace_bytes.argtypes = [_i32, _i32, _i32]
 _lib.ppas_plan_items.restype = _i32
 _lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
 _lib.ppas_step_plan_create.restype = ctypes.c_int
@@ -260,17 +262,25 @@ def attn_step_noalloc(shape: Shape, out, q, k_pages, v_pages, desc, bt_dev, bt_h
     _check(st, "ppas_attn_step_noalloc")
 
 
-def gateup_proj(x, w, y, events: Events | None = None, stream=None) -> None:
-    """y = x w^T: the fused gate-up projection (x [T, H], w [N, H], y [T, N], bf16 device tensors)."""
+def gateup_workspace_bytes(n_tokens: int, hidden: int, n_out: int) -> int:
+    return int(_lib.ppas_gateup_workspace_bytes(int(n_tokens), int(hidden), int(n_out)))
+
+
+def gateup_proj(x, w, y, workspace=None, events: Events | None = None, stream=None) -> None:
+    """y = x w^T: the fused gate-up projection (x [T, H], w [N, H], y [T, N], bf16 device tensors).
+    workspace: a device buffer for split reductions (see gateup_workspace_bytes), or None."""
     for t, name in ((x, "x"), (w, "w"), (y, "y")):
         if t.dim() != 2 or t.element_size() != 2:
             raise ValueError(f"{name} must be a 2-D bf16 tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
     T, H = x.shape
     N = w.shape[0]
     if w.shape[1] != H or tuple(y.shape) != (T, N):
         raise ValueError(f"shapes x {tuple(x.shape)}, w {tuple(w.shape)}, y {tuple(y.shape)} do not match")
-    st = _lib.ppas_gateup_proj(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N,
-                               None if events is None else ctypes.byref(events), _stream(stream))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.ppas_gateup_proj(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N, _dev(workspace, "workspace"),
+                               ws_bytes, None if events is None else ctypes.byref(events), _stream(stream))
     _check(st, "ppas_gateup_proj")
 
 

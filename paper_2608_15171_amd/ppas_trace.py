@@ -87,14 +87,67 @@ def bursty_requests(seed: int, n_bursts: int = 16, burst_size: int = 4, mean_gap
     return reqs
 
 
+def compose_iteration(live: list[Request], mode: str = "ppas", mbt: int = 16384, n_th: int = N_TH,
+                      b_max: int = B_MAX, b_cap: int = B_CAP):
+    """One scheduler iteration over the live (arrived, unfinished) requests, in arrival
+    order: returns (seqs, chunks, decodes, budget, n_p, n_d) with seqs the iteration's
+    descriptors (decode rows first), chunks the (request, tokens) prefill pieces and
+    decodes the requests given one decode token. Does not change the requests.
+
+    mode "ppas": prefill budget from Algorithm 1 under a global budget of mbt tokens.
+    mode "fixed": prefill budget is simply what mbt leaves after the decode tokens."""
+    prefills = [r for r in live if r.in_prefill]
+    decodes = [r for r in live if not r.in_prefill]
+    n_p, n_d = len(prefills), len(decodes)
+    if mode == "ppas":
+        budget = ppas_budget(n_p, n_d, n_th, b_max, b_cap)
+    elif mode == "fixed":
+        budget = mbt
+    else:
+        raise ValueError(mode)
+    seqs: list[Seq] = []
+    for r in decodes:
+        # the token generated last iteration is fed back at position L + g - 1
+        seqs.append(Seq(1, r.prompt_len + r.generated - 1, r.req_id))
+    room = min(budget, mbt - len(decodes))
+    # running prefills (already started) before waiting ones, each first-come first-served
+    order = [r for r in prefills if r.prefilled > 0] + [r for r in prefills if r.prefilled == 0]
+    chunks = []
+    for r in order:
+        if room <= 0:
+            break
+        take = min(r.prompt_len - r.prefilled, room)
+        chunks.append((r, take))
+        room -= take
+    for r, take in chunks:
+        seqs.append(Seq(take, r.prefilled, r.req_id))
+    return seqs, chunks, decodes, budget, n_p, n_d
+
+
+def apply_iteration(chunks, decodes) -> tuple[list, list]:
+    """Advance the requests by one executed iteration. Returns (first_token, completed):
+    the ids of requests that produced their first output token (last prompt chunk) and
+    of those that finished, in this iteration."""
+    first, completed = [], []
+    for r in decodes:
+        r.generated += 1
+        if r.finished:
+            completed.append(r.req_id)
+    for r, take in chunks:
+        r.prefilled += take
+        if not r.in_prefill:
+            r.generated = 1
+            first.append(r.req_id)
+            if r.finished:
+                completed.append(r.req_id)
+    return first, completed
+
+
 def run_trace(requests: list[Request], mode: str = "ppas", mbt: int = 16384,
               n_th: int = N_TH, b_max: int = B_MAX, b_cap: int = B_CAP,
               max_steps: int = 10_000_000) -> list[TraceStep]:
-    """Simulate the scheduler and return the non-empty iterations in order.
-
-    mode "ppas": prefill budget from Algorithm 1 under a global budget of mbt tokens.
-    mode "fixed": prefill budget is simply what mbt leaves after the decode tokens.
-    """
+    """Simulate the scheduler over iteration-indexed arrivals and return the non-empty
+    iterations in order (modes as in compose_iteration)."""
     reqs = sorted((Request(r.req_id, r.prompt_len, r.output_len, r.arrival_step) for r in requests),
                   key=lambda r: (r.arrival_step, r.req_id))
     arrived: list[Request] = []
@@ -109,43 +162,10 @@ def run_trace(requests: list[Request], mode: str = "ppas", mbt: int = 16384,
         if not live:
             t = reqs[nxt].arrival_step
             continue
-        prefills = [r for r in live if r.in_prefill]
-        decodes = [r for r in live if not r.in_prefill]
-        n_p, n_d = len(prefills), len(decodes)
-        if mode == "ppas":
-            budget = ppas_budget(n_p, n_d, n_th, b_max, b_cap)
-        elif mode == "fixed":
-            budget = mbt
-        else:
-            raise ValueError(mode)
-        seqs: list[Seq] = []
-        for r in decodes:
-            # the token generated last iteration is fed back at position L + g - 1
-            seqs.append(Seq(1, r.prompt_len + r.generated - 1, r.req_id))
-        room = min(budget, mbt - len(decodes))
-        # running prefills (already started) before waiting ones, each first-come first-served
-        order = [r for r in prefills if r.prefilled > 0] + [r for r in prefills if r.prefilled == 0]
-        chunks = []
-        for r in order:
-            if room <= 0:
-                break
-            take = min(r.prompt_len - r.prefilled, room)
-            chunks.append((r, take))
-            room -= take
-        for r, take in chunks:
-            seqs.append(Seq(take, r.prefilled, r.req_id))
+        seqs, chunks, decodes, budget, n_p, n_d = compose_iteration(live, mode, mbt, n_th, b_max, b_cap)
         step = TraceStep(t, StepSpec(f"trace-step{t}", seqs), n_p, n_d, budget,
                          prefill_tokens=sum(k for _, k in chunks), decode_rows=len(decodes))
-        for r in decodes:
-            r.generated += 1
-            if r.finished:
-                step.completed.append(r.req_id)
-        for r, take in chunks:
-            r.prefilled += take
-            if not r.in_prefill:
-                r.generated = 1
-                if r.finished:
-                    step.completed.append(r.req_id)
+        _, step.completed = apply_iteration(chunks, decodes)
         steps.append(step)
         t += 1
     return steps

@@ -164,15 +164,29 @@ def test_noalloc_refuses_oversized_steps_on_the_host():
 
 def test_gateup_proj_validates_before_any_device_work():
     f = ppas._lib.ppas_gateup_proj
-    assert f(1, 1, 1, 0, 64, 8, None, None) == ppas.PPAS_OK                 # no tokens: nothing to do
-    assert f(1, 1, 1, 4, 96, 8, None, None) == ppas.PPAS_EUNSUPPORTED       # hidden not a multiple of 64
-    assert f(1, 1, 1, -1, 64, 8, None, None) == ppas.PPAS_EINVAL
-    assert f(1, 1, 1, 4, 0, 8, None, None) == ppas.PPAS_EINVAL
-    assert f(1, 1, 1, 4, 64, 0, None, None) == ppas.PPAS_EINVAL
-    assert f(None, 1, 1, 4, 64, 8, None, None) == ppas.PPAS_EINVAL
-    assert f(1, 1, 1, 2 ** 31 - 1, 64, 8, None, None) == ppas.PPAS_ERANGE
+    assert f(1, 1, 1, 0, 64, 8, None, 0, None, None) == ppas.PPAS_OK                 # no tokens: nothing to do
+    assert f(1, 1, 1, 4, 96, 8, None, 0, None, None) == ppas.PPAS_EUNSUPPORTED       # hidden not a multiple of 64
+    assert f(1, 1, 1, -1, 64, 8, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 0, 8, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 64, 0, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(None, 1, 1, 4, 64, 8, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 64, 8, None, 1024, None, None) == ppas.PPAS_EINVAL         # workspace size without a buffer
+    assert f(1, 1, 1, 2 ** 31 - 1, 64, 8, None, 0, None, None) == ppas.PPAS_ERANGE
     half = ppas.events(start=1)
-    assert f(1, 1, 1, 4, 64, 8, ctypes.byref(half), None) == ppas.PPAS_EINVAL   # start without stop
+    assert f(1, 1, 1, 4, 64, 8, None, 0, ctypes.byref(half), None) == ppas.PPAS_EINVAL   # start without stop
+
+
+def test_gateup_workspace_sizing():
+    """Split reductions only when the 256 x 256 tiles are fewer than the compute units
+    (256 without a device): one tile row of 22016 columns does not split; a decode-sized
+    down projection (16 tokens, 11008 -> 2048: 8 tiles) splits 32 ways, a 2k chunk's
+    (64 tiles) 4 ways."""
+    W = ppas.gateup_workspace_bytes
+    assert W(2048, 2048, 22016) == 0
+    assert W(16, 11008, 2048) == 32 * 16 * 2048 * 4
+    assert W(2048, 11008, 2048) == 4 * 2048 * 2048 * 4
+    assert W(16, 2048, 2048) == 8 * 16 * 2048 * 4       # at least four 64-feature stages per split
+    assert W(0, 2048, 2048) == 0 and W(4, 96, 8) == 0
 
 
 def check_coverage(spec, items):

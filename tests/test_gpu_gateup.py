@@ -29,12 +29,16 @@ def lib():
     return ppas, step, torch
 
 
-def run(lib, xb, wb):
+def run(lib, xb, wb, split=True):
+    """split: give the call the workspace it asks for (reductions split across workgroups
+    when the output has fewer tiles than compute units); False: no workspace, no split."""
     ppas, step, torch = lib
     x = step.to_device_bf16(xb)
     w = step.to_device_bf16(wb)
     y = torch.full((xb.shape[0], wb.shape[0]), float("nan"), dtype=torch.bfloat16, device="cuda")
-    ppas.gateup_proj(x, w, y)
+    n = ppas.gateup_workspace_bytes(xb.shape[0], xb.shape[1], wb.shape[0]) if split else 0
+    ws = torch.full((max(n // 4, 1),), float("nan"), dtype=torch.float32, device="cuda") if n else None
+    ppas.gateup_proj(x, w, y, ws)
     torch.cuda.synchronize()
     return y
 
@@ -56,12 +60,26 @@ def f64(lib, y):
 
 
 @pytest.mark.parametrize("T,H,N", [(1, 64, 1), (5, 64, 300), (31, 128, 33), (257, 128, 513), (300, 192, 520),
-                                   (256, 256, 256), (513, 2048, 600), (700, 640, 1030)])
-def test_ragged_shapes_every_element(lib, T, H, N):
-    print(f"gate-up T={T} H={H} N={N}", flush=True)
+                                   (256, 256, 256), (513, 2048, 600), (700, 640, 1030),
+                                   # split reductions: the decoder layer's other projections at decode and
+                                   # chunk sizes (down 11008 -> 2048, QKV 2048 -> 2560, output 2048 -> 2048)
+                                   (16, 11008, 2048), (3, 11008, 2050), (100, 2048, 2560), (2048, 11008, 2048),
+                                   (600, 2048, 2048)])
+@pytest.mark.parametrize("split", [True, False])
+def test_ragged_shapes_every_element(lib, T, H, N, split):
+    ppas = lib[0]
+    print(f"gate-up T={T} H={H} N={N} split={split} workspace={ppas.gateup_workspace_bytes(T, H, N)}", flush=True)
     xb = I.gateup_tokens(1, T, 0, hidden=H)
     wb = I.gateup_weight(1, hidden=H, inter=(N + 1) // 2)[:N]
-    check(f64(lib, run(lib, xb, wb)), xb, wb, label=f"T{T} H{H} N{N}")
+    check(f64(lib, run(lib, xb, wb, split)), xb, wb, label=f"T{T} H{H} N{N} split={split}")
+
+
+def test_split_reduction_is_deterministic(lib):
+    ppas, step, torch = lib
+    xb = I.gateup_tokens(2, 40, 0, hidden=11008)
+    wb = I.gateup_weight(2, hidden=11008, inter=1024)
+    a, b = run(lib, xb, wb), run(lib, xb, wb)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
 def sample_rows(T):
