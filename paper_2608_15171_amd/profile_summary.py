@@ -49,6 +49,11 @@ ALGORITHMIC = {
 }
 
 
+def _sec(kernel: str) -> str:
+    """The attention workloads were profiled without the bench's secondary record."""
+    return " --secondary none" if kernel == "attn_step_kernel" else ""
+
+
 def sources_hash(sources) -> str:
     h = hashlib.sha256()
     for src in sources:
@@ -90,7 +95,7 @@ def main(workload: str, d: str, calib: str, kernel: str = "attn_step_kernel"):
            "write_factor": wfac, "fetch_kib": fetch_kib, "write_kib": write_kib}
     out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}")
     json.dump(rec, open(out + ".traffic.json", "w"), indent=1)
-    cmd = f"bench.py --workload {workload} --no-cpu-baseline"
+    cmd = f"bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline"
     lines = [f"# {kernel} -- workload {wl_name} ({workload})", "",
              DESCRIPTION[kernel], "",
              "## Kernel trace (rocprofv3 --kernel-trace --stats)", "", "Command:", "",
@@ -156,7 +161,7 @@ def mfma_summary(workload: str, d: str, kernel: str = "", simds: int = 1024, xcd
     busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (simds * cycles)
     mfma_flop = m["SQ_INSTS_MFMA"] * 32768       # the 32x32x16 bf16 and 16x16x32 bf16 MFMAs both do 2*16384 FLOP
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d <out> -o run "
-           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
     lines = [f"# {kernel} -- matrix-core utilisation, workload {bench['config']['workload']} ({workload})", "",
              DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
@@ -201,7 +206,7 @@ def stall_summary(workload: str, d: str, kernel: str = "", cus: int = 256, xcds:
     cycles = m["GRBM_GUI_ACTIVE"] / xcds
     wave = m["SQ_WAVE_CYCLES"]
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(STALL_COUNTERS)} --output-format csv -d <out> -o run "
-           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
     share = lambda k: f"{100 * m[k] / wave:.1f} % of wave time"
     lines = [f"# {kernel} -- where the waves spend their time, workload {bench['config']['workload']} ({workload})", "",
              DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
