@@ -509,7 +509,7 @@ ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_to
     if (gateup_tiles(n_tokens, n_out) * splits > INT32_MAX) splits = 1;
     const hipError_t e = launch_gateup(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
                                        static_cast<uint16_t*>(y), n_tokens, hidden, n_out, splits,
-                                       static_cast<float*>(workspace), static_cast<hipStream_t>(hip_stream),
+                                       static_cast<float*>(workspace), dev.cus, static_cast<hipStream_t>(hip_stream),
                                        ev_of(events, 0), ev_of(events, 1));
     return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
   } catch (...) {

@@ -13,19 +13,22 @@
 // row), into a two-slot ring. In LDS a row keeps its eight 16-byte chunks in
 // an XOR-swizzled order, so each operand fragment read (row tile, k-step: 32
 // rows x 32 bytes) is one bank-conflict-free ds_read_b128, and each fragment
-// feeds four MFMAs. The next stage's transfers are issued a quarter per k-step
-// behind the operand reads, and the next k-step's fragments are read while the
-// current k-step's 16 MFMAs run. (Transfers of 32-byte row pieces straight into
-// operand order, and rings of four 32-feature stages, measured 33 % and 6 %
-// slower.)
+// feeds four MFMAs. The next stage's transfers are issued in the first two of
+// the stage's four k-steps, and the next k-step's fragments are read in two
+// groups while the current k-step's 16 MFMAs run. (Transfers of 32-byte row
+// pieces straight into operand order, and rings of four or five 32-feature
+// stages, measured 33 %, 6 % and 2 % slower; transfers spread over all four
+// k-steps 4 % slower, issued in one k-step 8 % slower, or interleaved one by one
+// with the MFMAs no faster.)
 //
 // The MFMA's first operand is W (rows = output columns), its second X (rows =
 // tokens): lane L of a 32 x 32 result then holds token row L % 32 and, in
 // registers 4g..4g+3, four consecutive output columns 8g + 4(L / 32) + 0..3,
 // which the epilogue packs into 8-byte LDS writes; the tile then leaves LDS as
-// 256-byte row runs of 16-byte stores.
+// 256-byte row runs of 16-byte stores, eight LDS reads ahead of their stores.
 //
-// Tile order. Workgroup b runs on XCD b % 8; each XCD takes a contiguous range
+// Tile order. The grid holds one workgroup per compute unit, each looping over
+// its tiles. Workgroup b runs on XCD b % 8; each XCD takes a contiguous range
 // of tiles, and tiles are numbered in groups of 8 token-row tiles that share a
 // weight tile, so the workgroups resident on one XCD share operand tiles in
 // that XCD's L2.
@@ -56,6 +59,9 @@ typedef __attribute__((address_space(1))) const void global_cvoid;
 #ifndef PPAS_GATEUP_RING
 #define PPAS_GATEUP_RING 2
 #endif
+#ifndef PPAS_GATEUP_SPREAD
+#define PPAS_GATEUP_SPREAD 2
+#endif
 constexpr int kThreads = 256;
 constexpr int kBM = 256;                 // token rows per tile
 constexpr int kBMTail = 64;              // token rows per tile of the last T % 256 rows
@@ -70,11 +76,18 @@ constexpr int kPart = 256 * kRowBytes;   // the 256 W (or X) rows of one stage
 constexpr int kStage = 2 * kPart;
 constexpr int kDmaPerStage = 128 / kRowsPerDma;   // transfers per wave per stage (two waves per part)
 static_assert(kBK == 32 || kBK == 64, "stages of 32 or 64 features");
-static_assert(kRing >= 2 && kRing <= 4, "a ring of two to four stages");
+static_assert(kRing >= 2 && kRing <= 5, "a ring of two to five stages");
+constexpr int kSpread = PPAS_GATEUP_SPREAD < kKSteps ? PPAS_GATEUP_SPREAD : kKSteps;   // k-steps that issue the next stage
 constexpr int kPitch = 128 * 2 + 16;     // epilogue LDS row pitch in bytes (16-byte aligned, padded)
 constexpr int kEpiWave = 128 * kPitch;   // one wave's 128 x 128 bf16 output block
 constexpr int kSmem = (kRing * kStage > 4 * kEpiWave) ? kRing * kStage : 4 * kEpiWave;
+static_assert(kSmem <= 160 * 1024, "the LDS of one compute unit");
 constexpr int kGroupM = 8;               // token-row tiles per tile-order group
+#ifndef PPAS_GATEUP_PERSIST
+#define PPAS_GATEUP_PERSIST 1
+#endif
+constexpr bool kPersist = PPAS_GATEUP_PERSIST;   // a workgroup per compute unit, looping over tiles
+
 
 struct GemmArgs {
   const uint16_t* x;
@@ -108,6 +121,26 @@ __device__ __forceinline__ void dma16(const uint16_t* g, char* lds) {
 }
 
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Wait until at most `later` stages of PER transfers each are still in flight
+// (vmcnt: bits 3:0 and 15:14 of the s_waitcnt immediate).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+template <int PER>
+__device__ __forceinline__ void wait_stages(int later) {
+  static_assert((kRing - 2) * PER < 64, "the transfers in flight fit the vmcnt counter");
+  if (later >= 3)
+    wait_vmcnt<(kRing >= 5 ? 3 * PER : 0)>();
+  else if (later == 2)
+    wait_vmcnt<2 * PER>();
+  else if (later == 1)
+    wait_vmcnt<PER>();
+  else
+    wait_vmcnt<0>();
+}
 
 // Workgroup barrier without a memory fence (the fence of __syncthreads would also
 // wait for the transfers still in flight for later stages). The LDS data it
@@ -144,7 +177,6 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
   const bool is_x = w >= 2;
   const int half = w & 1;
   const int rows_half = is_x ? BM / 2 : 128;
-  const int ndma = is_x ? kDmaX : kDmaMax;
   const uint16_t* gptr[kDmaMax];
   {
     const uint16_t* base = is_x ? a.x : a.w;
@@ -172,15 +204,15 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
     else
       issue(s, 0, std::integral_constant<int, kDmaMax>{});
   };
-  // a quarter of the stage's transfers per k-step
-  auto issue_part = [&](int s, int j) {
-    if (is_x)
-      issue(s, j * (kDmaX / kKSteps), std::integral_constant<int, kDmaX / kKSteps>{});
-    else
-      issue(s, j * (kDmaMax / kKSteps), std::integral_constant<int, kDmaMax / kKSteps>{});
+  // transfer i of this wave for stage sd into ring slot `slot` (in tail tiles
+  // the X waves have fewer transfers than the W waves)
+  auto dma_one = [&](int sd, int slot, int i) {
+    if (kDmaX == kDmaMax || !is_x || i < kDmaX)
+      dma16(gptr[i] + sd * kBK, smem + slot * kStage + dst0 + i * kRowsPerDma * kRowBytes);
   };
-  static_assert(kDmaX % kKSteps == 0 && kDmaMax % kKSteps == 0, "transfers split evenly over the k-steps");
-  (void)ndma;
+  constexpr int kDmaStep = kDmaMax / kSpread;   // transfers per k-step in the first kSpread k-steps
+  static_assert(kDmaMax % kSpread == 0 && (kDmaX % kDmaStep == 0 || kDmaX < kDmaStep),
+                "transfers split evenly over the k-steps");
 
   const int wn = w >> 1, wm = w & 1;
   f32x16 acc[4][kMT];
@@ -201,57 +233,96 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
 #pragma unroll
   for (int s = 0; s < kRing - 1; ++s)
     if (k_lo + s < k_hi) issue_all(k_lo + s);
-  for (int s = k_lo; s < k_hi; ++s) {
-    // this wave's transfers of stage s are done once at most those of the stages
-    // after it (up to two) are still in flight; the barrier then makes every
-    // wave's part visible and tells that stage s - 1, whose ring slot the next
-    // transfers overwrite, has been read by all waves
+
+  // Entering stage s: this wave's transfers of stage s are done once at most
+  // those of the stages after it are still in flight; the barrier then makes
+  // every wave's part visible and tells that stage s - 1, whose ring slot the
+  // next transfers overwrite, has been read by all waves.
+  auto enter = [&](int s) {
     const int later = min(k_hi - 1 - s, kRing - 2);
-    const int per = is_x ? kDmaX : kDmaMax;
-    if (later >= 2) {
-      if (per == 16)
-        __builtin_amdgcn_s_waitcnt(0x0F70 | ((32) & 15) | (((32) >> 4) << 14));
-      else
-        __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * kDmaX) & 15) | (((2 * kDmaX) >> 4) << 14));
-    } else if (later == 1) {
-      if (per == 16)
-        __builtin_amdgcn_s_waitcnt(0x0F70 | (16 & 15) | ((16 >> 4) << 14));
-      else
-        __builtin_amdgcn_s_waitcnt(0x0F70 | (kDmaX & 15) | ((kDmaX >> 4) << 14));
-    } else {
-      wait_vmem();
-    }
+    if (is_x)
+      wait_stages<kDmaX>(later);
+    else
+      wait_stages<kDmaMax>(later);
     bare_barrier();
-    const bool more = s + kRing - 1 < k_hi;
+  };
+  // Operand fragments, double-buffered over k-steps. A k-step's eight reads go
+  // out in two groups, (W 0, W 1, X 0 .. kMT-1) and (W 2, W 3), the first ahead
+  // of the previous k-step's MFMAs and the second halfway through them, so that
+  // at most 14 reads are outstanding (the LDS wait counter holds 15; with more
+  // in flight every wait would have to drain them all).
+  bf16x8 fa[2][4], fb[2][kMT];
+  auto stage_ptrs = [&](int s, const char*& wf, const char*& xf) {
     const char* cur = smem + (s % kRing) * kStage;
-    const char* wf = cur + 128 * wn * kRowBytes;
-    const char* xf = cur + kPart + (BM / 2) * wm * kRowBytes;
-    // The fragments of k-step j + 1 are read while the MFMAs of k-step j run (the
-    // scheduling barriers keep the reads ahead of those MFMAs).
-    bf16x8 fa[2][4], fb[2][kMT];
-    auto read = [&](int j, bf16x8 (&ra)[4], bf16x8 (&rb)[kMT]) {
+    wf = cur + 128 * wn * kRowBytes;
+    xf = cur + kPart + (BM / 2) * wm * kRowBytes;
+  };
+  auto read_a = [&](int s, int j, int f) {
+    const char *wf, *xf;
+    stage_ptrs(s, wf, xf);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) ra[q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+    for (int q = 0; q < 2; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
 #pragma unroll
-      for (int q = 0; q < kMT; ++q) rb[q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
-    };
-    read(0, fa[0], fb[0]);
+    for (int q = 0; q < kMT; ++q) fb[f][q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
+  };
+  auto read_b = [&](int s, int j, int f) {
+    const char *wf, *xf;
+    stage_ptrs(s, wf, xf);
+#pragma unroll
+    for (int q = 2; q < 4; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+  };
+  constexpr int kN = 4 * kMT;   // MFMAs per k-step: W row tile idx / kMT, X row tile idx % kMT
+  static_assert(kKSteps % 2 == 0, "k-steps alternate the two fragment buffers");
+
+  if (k_lo < k_hi) {
+    enter(k_lo);
+    read_a(k_lo, 0, 0);
+    read_b(k_lo, 0, 0);
+  }
+  for (int s = k_lo; s < k_hi; ++s) {
+    // The transfers of stage s + kRing - 1 go into the slot of stage s - 1, which
+    // every wave has finished reading (the barrier of entering s). Past the last
+    // stage they repeat stage k_hi - 1 into that free slot, which keeps the loop
+    // free of branches around them; the waits count them as stages in flight.
+    const int sd = min(s + kRing - 1, k_hi - 1);
+    const int slot = (s + kRing - 1) % kRing;
 #pragma unroll
     for (int j = 0; j < kKSteps; ++j) {
-      if (j + 1 < kKSteps) read(j + 1, fa[(j + 1) & 1], fb[(j + 1) & 1]);
-      // the next stage's transfers, a quarter per k-step, issued behind this
-      // k-step's operand reads so that the matrix cores start without waiting
-      // for the whole batch of transfers
-      if (more) issue_part(s + kRing - 1, j);
-      __builtin_amdgcn_sched_barrier(0);
+      const int f = j & 1;
+      const bool last = j + 1 == kKSteps;
+      if (!last) read_a(s, j + 1, f ^ 1);
+      // this k-step's share of the next stage's transfers, behind the operand
+      // reads so that the matrix cores start without waiting for them
+      if (j < kSpread) {
 #pragma unroll
-      for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-        for (int tj = 0; tj < kMT; ++tj)
-          acc[ti][tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[j & 1][ti], fb[j & 1][tj], acc[ti][tj], 0, 0, 0);
+        for (int d = 0; d < kDmaStep; ++d) dma_one(sd, slot, j * kDmaStep + d);
+      }
       __builtin_amdgcn_sched_barrier(0);
+      // the MFMAs, with the second read group halfway
+#pragma unroll
+      for (int idx = 0; idx < kN; ++idx) {
+        const int ti = idx / kMT, tj = idx % kMT;
+        acc[ti][tj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[f][ti], fb[f][tj], acc[ti][tj], 0, 0, 0);
+        if (!last && idx == kN / 2 - 1) {
+          __builtin_amdgcn_sched_barrier(0);
+          read_b(s, j + 1, f ^ 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (last) {
+        if (s + 1 < k_hi) {
+          enter(s + 1);
+          read_a(s + 1, 0, 0);
+          read_b(s + 1, 0, 0);
+        }
+        // (outside the condition: a scheduling barrier inside it made the
+        // register allocator spill)
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
+  wait_vmem();   // the repeated transfers of the last stages have landed
   __syncthreads();   // every wave is done with the ring before it holds the output
 
   // Result register r of MFMA tile (ti, tj): token row 32 tj + L % 32 of the
@@ -301,6 +372,20 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
       }
   __syncthreads();
   const int nb = nw + 8 * (lane & 15);
+  if (mw + BM / 2 <= a.T && nw + 128 <= a.N2) {
+    // interior block: eight LDS reads in flight, then their eight stores
+#pragma unroll
+    for (int s0 = 0; s0 < BM / 8; s0 += 8) {
+      u32x4 v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = lds16(eb + (4 * (s0 + i) + (lane >> 4)) * kPitch + 16 * (lane & 15));
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        *reinterpret_cast<u32x4*>(a.y + size_t(mw + 4 * (s0 + i) + (lane >> 4)) * a.N2 + nb) = v[i];
+      }
+    }
+    return;
+  }
 #pragma unroll 4
   for (int s = 0; s < BM / 8; ++s) {
     const int row = 4 * s + (lane >> 4);
@@ -321,33 +406,40 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
 __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kSmem];
 
-  // blockIdx -> (tile, split): the first 8 * (items / 8) workgroups give XCD b % 8
-  // the contiguous range of items xcd * (items / 8) + ...; the remainder runs in
-  // order. Item u is tile u % tiles of reduction split u / tiles, so the
-  // workgroups next to each other on an XCD work on neighbouring tiles of the
-  // same split. Tiles 0 .. full - 1 are the 256-row tiles (in groups of 8 that
-  // share a weight tile), the rest the 64-row tiles of the last T % 256 rows.
+  // Work item q -> (tile, split): the first 8 * (items / 8) items give XCD q % 8
+  // the contiguous range xcd * (items / 8) + q / 8 (workgroup b runs on XCD b % 8,
+  // and the grid is a multiple of 8 whenever it is smaller than the item count);
+  // the remainder runs in order. Item u is tile u % tiles of reduction split
+  // u / tiles, so the workgroups next to each other on an XCD work on
+  // neighbouring tiles of the same split. Tiles 0 .. full - 1 are the 256-row
+  // tiles (in groups of 8 that share a weight tile), the rest the 64-row tiles of
+  // the last T % 256 rows. A workgroup takes items blockIdx.x, + gridDim.x, ...
   const int full = a.tiles_m * a.tiles_n;
   const int ntiles = full + a.tail_m * a.tiles_n;
   const int nitems = ntiles * a.splits;
   const int per_xcd = nitems / 8;
-  const int b = blockIdx.x;
-  const int u = (b < 8 * per_xcd) ? (b % 8) * per_xcd + b / 8 : b;
-  const int t = u % ntiles;
-  const int split = u / ntiles;
   const int nk_all = a.H / kBK;
-  const int k_lo = int(int64_t(split) * nk_all / a.splits);
-  const int k_hi = int(int64_t(split + 1) * nk_all / a.splits);
-  if (t < full) {
-    const int grp = t / (kGroupM * a.tiles_n);
-    const int first_m = grp * kGroupM;
-    const int gm = min(kGroupM, a.tiles_m - first_m);
-    const int in_grp = t - grp * kGroupM * a.tiles_n;
-    tile_body<kBM>(a, smem, (first_m + in_grp % gm) * kBM, (in_grp / gm) * kBN, split, k_lo, k_hi);
-  } else {
-    const int tt = t - full;
-    tile_body<kBMTail>(a, smem, a.tiles_m * kBM + (tt % a.tail_m) * kBMTail, (tt / a.tail_m) * kBN, split, k_lo,
-                       k_hi);
+  for (int q = blockIdx.x; q < nitems; q += gridDim.x) {
+    const int u = (q < 8 * per_xcd) ? (q % 8) * per_xcd + q / 8 : q;
+    const int t = u % ntiles;
+    const int split = u / ntiles;
+    const int k_lo = int(int64_t(split) * nk_all / a.splits);
+    const int k_hi = int(int64_t(split + 1) * nk_all / a.splits);
+    if (t < full) {
+      const int grp = t / (kGroupM * a.tiles_n);
+      const int first_m = grp * kGroupM;
+      const int gm = min(kGroupM, a.tiles_m - first_m);
+      const int in_grp = t - grp * kGroupM * a.tiles_n;
+      tile_body<kBM>(a, smem, (first_m + in_grp % gm) * kBM, (in_grp / gm) * kBN, split, k_lo, k_hi);
+    } else {
+      const int tt = t - full;
+      tile_body<kBMTail>(a, smem, a.tiles_m * kBM + (tt % a.tail_m) * kBMTail, (tt / a.tail_m) * kBN, split,
+                         k_lo, k_hi);
+    }
+    // the next item's transfers overwrite the LDS this item's epilogue has read;
+    // its stores may still be in flight
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    bare_barrier();
   }
 }
 
@@ -392,7 +484,8 @@ size_t gateup_workspace_bytes(int32_t T, int32_t N2, int splits) {
 }
 
 hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t T, int32_t H, int32_t N2,
-                         int splits, float* part, hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop) {
+                         int splits, float* part, int cus, hipStream_t stream, hipEvent_t ev_start,
+                         hipEvent_t ev_stop) {
   GemmArgs a;
   a.x = x;
   a.w = w;
@@ -408,7 +501,11 @@ hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int3
   const int64_t n = gateup_tiles(T, N2) * splits;
   if (n <= 0) return hipSuccess;
   if (n > INT32_MAX || splits < 1 || splits > H / kBK || (splits > 1 && !part)) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL(gateup_kernel, dim3(unsigned(n)), dim3(kThreads), 0, stream, ev_start,
+  // one workgroup per compute unit, each looping over its items (a multiple of 8
+  // workgroups, so that every workgroup stays on one XCD's share of the items)
+  const int64_t slots = kPersist ? std::max(8, cus / 8 * 8) : n;
+  const int64_t grid = std::min<int64_t>(n, slots);
+  hipExtLaunchKernelGGL(gateup_kernel, dim3(unsigned(grid)), dim3(kThreads), 0, stream, ev_start,
                         splits > 1 ? nullptr : ev_stop, 0, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
