@@ -4,28 +4,31 @@
 // (nearest even). W stacks the gate rows over the up rows, so one launch
 // computes both projections of a prefill chunk.
 //
-// Tiling. A workgroup of four waves (one per SIMD) computes a 256 x 256 output
-// tile; wave (wn, wm) owns its 128 output columns x 128 token rows as 4 x 4
-// MFMA tiles (256 fp32 accumulators per lane, held in the accumulation
-// registers). The reduction advances 64 features per stage: a stage's W rows
-// and X rows (32 KB each) are copied into LDS by 16-byte global-to-LDS
-// transfers, each covering eight whole 128-byte row runs (one cache line per
-// row), into a two-slot ring. In LDS a row keeps its eight 16-byte chunks in
-// an XOR-swizzled order, so each operand fragment read (row tile, k-step: 32
-// rows x 32 bytes) is one bank-conflict-free ds_read_b128, and each fragment
-// feeds four MFMAs. The next stage's transfers are issued in the first two of
-// the stage's four k-steps, and the next k-step's fragments are read in two
-// groups while the current k-step's 16 MFMAs run. (Transfers of 32-byte row
-// pieces straight into operand order, and rings of four or five 32-feature
-// stages, measured 33 %, 6 % and 2 % slower; transfers spread over all four
-// k-steps 4 % slower, issued in one k-step 8 % slower, or interleaved one by one
-// with the MFMAs no faster.)
+// Tiling. A workgroup of eight waves (two per SIMD) computes a 256 x 256
+// output tile; wave (wn, wm) owns 128 output columns x 64 token rows as 4 x 2
+// MFMA tiles (128 fp32 accumulators per lane), so that while one wave of a SIMD
+// waits (its transfers' issue, an LDS read) the other keeps the matrix core
+// busy. (Four waves of 128 x 128, one per SIMD with 256 accumulators each,
+// read half as many LDS bytes per MFMA but measured 5 % slower.) The reduction
+// advances 64 features per stage: a stage's W rows and X rows (32 KB each) are
+// copied into LDS by 16-byte global-to-LDS transfers, each covering eight whole
+// 128-byte row runs (one cache line per row), into a two-slot ring. In LDS a
+// row keeps its eight 16-byte chunks in an XOR-swizzled order, so each operand
+// fragment read (row tile, k-step: 32 rows x 32 bytes) is one bank-conflict-free
+// ds_read_b128. The next stage's transfers are issued in the first two of the
+// stage's four k-steps, and the next k-step's fragments are read in two groups
+// while the current k-step's MFMAs run. (Transfers of 32-byte row pieces
+// straight into operand order, and rings of four or five 32-feature stages,
+// measured 33 %, 6-13 % and 2-12 % slower; transfers spread over all four
+// k-steps 4-7 % slower, issued in one k-step 2-8 % slower, or interleaved one by
+// one with the MFMAs no faster.)
 //
 // The MFMA's first operand is W (rows = output columns), its second X (rows =
 // tokens): lane L of a 32 x 32 result then holds token row L % 32 and, in
 // registers 4g..4g+3, four consecutive output columns 8g + 4(L / 32) + 0..3,
-// which the epilogue packs into 8-byte LDS writes; the tile then leaves LDS as
-// 256-byte row runs of 16-byte stores, eight LDS reads ahead of their stores.
+// which the epilogue packs into 8-byte LDS writes; the wave's block then leaves
+// LDS as 256-byte row runs of 16-byte stores, eight LDS reads ahead of their
+// stores.
 //
 // Tile order. The grid holds one workgroup per compute unit, each looping over
 // its tiles. Workgroup b runs on XCD b % 8; each XCD takes a contiguous range
@@ -62,7 +65,12 @@ typedef __attribute__((address_space(1))) const void global_cvoid;
 #ifndef PPAS_GATEUP_SPREAD
 #define PPAS_GATEUP_SPREAD 2
 #endif
-constexpr int kThreads = 256;
+#ifndef PPAS_GATEUP_WAVES
+#define PPAS_GATEUP_WAVES 8
+#endif
+constexpr int kWaves = PPAS_GATEUP_WAVES;  // waves per workgroup: one or two per SIMD
+static_assert(kWaves == 4 || kWaves == 8, "four or eight waves");
+constexpr int kThreads = 64 * kWaves;
 constexpr int kBM = 256;                 // token rows per tile
 constexpr int kBMTail = 64;              // token rows per tile of the last T % 256 rows
 constexpr int kBN = 256;                 // output columns per tile
@@ -74,13 +82,12 @@ constexpr int kRowBytes = 16 * kCPR;
 constexpr int kRowsPerDma = 64 / kCPR;   // whole rows covered by one 64-lane 16-byte transfer
 constexpr int kPart = 256 * kRowBytes;   // the 256 W (or X) rows of one stage
 constexpr int kStage = 2 * kPart;
-constexpr int kDmaPerStage = 128 / kRowsPerDma;   // transfers per wave per stage (two waves per part)
 static_assert(kBK == 32 || kBK == 64, "stages of 32 or 64 features");
 static_assert(kRing >= 2 && kRing <= 5, "a ring of two to five stages");
 constexpr int kSpread = PPAS_GATEUP_SPREAD < kKSteps ? PPAS_GATEUP_SPREAD : kKSteps;   // k-steps that issue the next stage
 constexpr int kPitch = 128 * 2 + 16;     // epilogue LDS row pitch in bytes (16-byte aligned, padded)
-constexpr int kEpiWave = 128 * kPitch;   // one wave's 128 x 128 bf16 output block
-constexpr int kSmem = (kRing * kStage > 4 * kEpiWave) ? kRing * kStage : 4 * kEpiWave;
+constexpr int kEpiWave = (kBM * 2 / kWaves) * kPitch;   // one wave's output block of a full tile (<= 128 columns)
+constexpr int kSmem = (kRing * kStage > kWaves * kEpiWave) ? kRing * kStage : kWaves * kEpiWave;
 static_assert(kSmem <= 160 * 1024, "the LDS of one compute unit");
 constexpr int kGroupM = 8;               // token-row tiles per tile-order group
 #ifndef PPAS_GATEUP_PERSIST
@@ -157,26 +164,35 @@ __device__ __forceinline__ void bare_barrier() {
 
 // One output tile of BM token rows x 256 columns over stages k_lo .. k_hi - 1.
 // BM = 256 (full tiles) or 64 (the ragged last rows of the tokens, and calls of
-// fewer than 256 tokens): wave (wn, wm) owns 128 columns x BM / 2 rows, i.e.
-// 4 x BM / 64 MFMA tiles. The W part of a stage is always 256 rows (waves 0 and
-// 1 copy 128 each), the X part BM rows (waves 2 and 3 copy BM / 2 each).
+// fewer than 256 tokens). Wave (wn, wm) owns a WN x WM block of it (columns x
+// token rows) as kNT x kMT MFMA tiles of 32 x 32:
+//   four waves:  128 x 128 (full), 128 x 32 (tail)
+//   eight waves: 128 x 64 (full),   64 x 32 (tail)
+// The W part of a stage is always 256 rows, the X part BM rows; the first half
+// of the waves copy the W part, the second half the X part, in equal shares.
 template <int BM>
 __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0, int n0, int split, int k_lo,
                                           int k_hi) {
-  constexpr int kMT = BM / 64;                       // MFMA row tiles of a wave in the token dimension
-  constexpr int kDmaX = (BM / 2) / kRowsPerDma;      // transfers per X wave per stage
-  constexpr int kDmaMax = kDmaPerStage;              // a W wave's count (the larger)
+  constexpr int WN = (BM == kBM || kWaves == 4) ? 128 : 64;   // columns per wave
+  constexpr int NG = kBN / WN;                                // column groups
+  constexpr int WM = BM / (kWaves / NG);                      // token rows per wave
+  constexpr int kNT = WN / 32, kMT = WM / 32;                 // MFMA tiles per wave
+  static_assert(NG * (BM / WM) == kWaves && WM % 32 == 0, "wave blocks tile the output tile");
+  constexpr int kHalf = kWaves / 2;                  // waves per operand part
+  constexpr int kDmaX = (BM / kHalf) / kRowsPerDma;  // transfers per X wave per stage
+  constexpr int kDmaMax = (kBN / kHalf) / kRowsPerDma;   // a W wave's count (the larger)
+  static_assert(kDmaX >= 1, "every X wave copies whole transfers");
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-  // Transfers: wave w copies half of one part of every stage: W rows (waves 0, 1)
-  // or X rows (waves 2, 3). One transfer covers kRowsPerDma whole rows (the row's
-  // 16-byte chunks spread over kCPR consecutive lanes); lane L lands at 16 L, i.e.
-  // at row position L % kCPR of its row, and fetches the chunk stored there under
-  // the swizzle.
-  const bool is_x = w >= 2;
-  const int half = w & 1;
-  const int rows_half = is_x ? BM / 2 : 128;
+  // Transfers: wave w copies its share of one part of every stage: W rows (the
+  // first half of the waves) or X rows (the second half). One transfer covers
+  // kRowsPerDma whole rows (the row's 16-byte chunks spread over kCPR consecutive
+  // lanes); lane L lands at 16 L, i.e. at row position L % kCPR of its row, and
+  // fetches the chunk stored there under the swizzle.
+  const bool is_x = w >= kHalf;
+  const int half = w % kHalf;
+  const int rows_half = is_x ? BM / kHalf : kBN / kHalf;
   const uint16_t* gptr[kDmaMax];
   {
     const uint16_t* base = is_x ? a.x : a.w;
@@ -214,10 +230,10 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
   static_assert(kDmaMax % kSpread == 0 && (kDmaX % kDmaStep == 0 || kDmaX < kDmaStep),
                 "transfers split evenly over the k-steps");
 
-  const int wn = w >> 1, wm = w & 1;
-  f32x16 acc[4][kMT];
+  const int wn = w % NG, wm = w / NG;
+  f32x16 acc[kNT][kMT];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kNT; ++i)
 #pragma unroll
     for (int j = 0; j < kMT; ++j)
 #pragma unroll
@@ -251,17 +267,17 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
   // of the previous k-step's MFMAs and the second halfway through them, so that
   // at most 14 reads are outstanding (the LDS wait counter holds 15; with more
   // in flight every wait would have to drain them all).
-  bf16x8 fa[2][4], fb[2][kMT];
+  bf16x8 fa[2][kNT], fb[2][kMT];
   auto stage_ptrs = [&](int s, const char*& wf, const char*& xf) {
     const char* cur = smem + (s % kRing) * kStage;
-    wf = cur + 128 * wn * kRowBytes;
-    xf = cur + kPart + (BM / 2) * wm * kRowBytes;
+    wf = cur + WN * wn * kRowBytes;
+    xf = cur + kPart + WM * wm * kRowBytes;
   };
   auto read_a = [&](int s, int j, int f) {
     const char *wf, *xf;
     stage_ptrs(s, wf, xf);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+    for (int q = 0; q < kNT / 2; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
 #pragma unroll
     for (int q = 0; q < kMT; ++q) fb[f][q] = as_bf16x8(lds16(xf + 32 * q * kRowBytes + roff[j]));
   };
@@ -269,9 +285,9 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
     const char *wf, *xf;
     stage_ptrs(s, wf, xf);
 #pragma unroll
-    for (int q = 2; q < 4; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
+    for (int q = kNT / 2; q < kNT; ++q) fa[f][q] = as_bf16x8(lds16(wf + 32 * q * kRowBytes + roff[j]));
   };
-  constexpr int kN = 4 * kMT;   // MFMAs per k-step: W row tile idx / kMT, X row tile idx % kMT
+  constexpr int kN = kNT * kMT;   // MFMAs per k-step: W row tile idx / kMT, X row tile idx % kMT
   static_assert(kKSteps % 2 == 0, "k-steps alternate the two fragment buffers");
 
   if (k_lo < k_hi) {
@@ -327,13 +343,13 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
 
   // Result register r of MFMA tile (ti, tj): token row 32 tj + L % 32 of the
   // wave's rows, column 32 ti + 8(r / 4) + 4(L / 32) + r % 4 of its columns.
-  const int mw = m0 + (BM / 2) * wm, nw = n0 + 128 * wn;
+  const int mw = m0 + WM * wm, nw = n0 + WN * wn;
   if (a.splits > 1) {
     // fp32 partial sums of this split, straight from the accumulators: four
     // consecutive columns of one token row per (ti, tj, g)
     float* pb = a.part + size_t(split) * a.T * a.N2;
 #pragma unroll
-    for (int ti = 0; ti < 4; ++ti)
+    for (int ti = 0; ti < kNT; ++ti)
 #pragma unroll
       for (int tj = 0; tj < kMT; ++tj) {
         const int m = mw + 32 * tj + (lane & 31);
@@ -355,10 +371,11 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
     return;
   }
 
-  // bf16: the wave's block to LDS (token-row major), then out in 256-byte row runs.
+  // bf16: the wave's block to LDS (token-row major), then out in WN * 2-byte row
+  // runs (kLPR lanes per row, kRPI rows per store instruction).
   char* eb = smem + w * kEpiWave;
 #pragma unroll
-  for (int ti = 0; ti < 4; ++ti)
+  for (int ti = 0; ti < kNT; ++ti)
 #pragma unroll
     for (int tj = 0; tj < kMT; ++tj)
 #pragma unroll
@@ -371,27 +388,29 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
         *reinterpret_cast<u32x2*>(eb + row * kPitch + col * 2) = v;
       }
   __syncthreads();
-  const int nb = nw + 8 * (lane & 15);
-  if (mw + BM / 2 <= a.T && nw + 128 <= a.N2) {
-    // interior block: eight LDS reads in flight, then their eight stores
+  constexpr int kLPR = WN / 8, kRPI = 64 / kLPR, kIters = WM / kRPI;
+  const int nb = nw + 8 * (lane % kLPR);
+  if (mw + WM <= a.T && nw + WN <= a.N2) {
+    // interior block: up to eight LDS reads in flight, then their stores
+    constexpr int kB = kIters < 8 ? kIters : 8;
 #pragma unroll
-    for (int s0 = 0; s0 < BM / 8; s0 += 8) {
-      u32x4 v[8];
+    for (int s0 = 0; s0 < kIters; s0 += kB) {
+      u32x4 v[kB];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = lds16(eb + (4 * (s0 + i) + (lane >> 4)) * kPitch + 16 * (lane & 15));
+      for (int i = 0; i < kB; ++i)
+        v[i] = lds16(eb + (kRPI * (s0 + i) + lane / kLPR) * kPitch + 16 * (lane % kLPR));
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        *reinterpret_cast<u32x4*>(a.y + size_t(mw + 4 * (s0 + i) + (lane >> 4)) * a.N2 + nb) = v[i];
-      }
+      for (int i = 0; i < kB; ++i)
+        *reinterpret_cast<u32x4*>(a.y + size_t(mw + kRPI * (s0 + i) + lane / kLPR) * a.N2 + nb) = v[i];
     }
     return;
   }
 #pragma unroll 4
-  for (int s = 0; s < BM / 8; ++s) {
-    const int row = 4 * s + (lane >> 4);
+  for (int s = 0; s < kIters; ++s) {
+    const int row = kRPI * s + lane / kLPR;
     const int m = mw + row;
     if (m >= a.T) break;
-    const u32x4 v = lds16(eb + row * kPitch + 16 * (lane & 15));
+    const u32x4 v = lds16(eb + row * kPitch + 16 * (lane % kLPR));
     uint16_t* dst = a.y + size_t(m) * a.N2 + nb;
     if (nb + 8 <= a.N2) {
       *reinterpret_cast<u32x4*>(dst) = v;
