@@ -5,7 +5,9 @@ give weight row sums, rank-one inputs factor), invariants (token rows are
 independent, so any chunking of a prompt gives the same rows -- the property the
 paper's 8 x 2k vs 1 x 16k comparison rests on; the gate and up halves are
 independent projections; integer-valued inputs are exactly linear), and planted
-mistakes that the pins must reject."""
+mistakes that the pins must reject. The gated activation (gate_up_act) is pinned
+by a brute force with math.exp, the identity silu(g) - silu(-g) = g, its limits,
+and zero halves."""
 import math
 import struct
 import types
@@ -126,6 +128,74 @@ def test_abs_product_bounds_the_product():
     np.testing.assert_allclose(y2, a2, rtol=1e-14, atol=0)
 
 
+# ------------------------------------------------------------- gated activation
+
+def silu_math(g):
+    """g * sigmoid(g) with math.exp, written for both signs without overflow."""
+    if g >= 0:
+        return g / (1.0 + math.exp(-g))
+    e = math.exp(g)
+    return g * e / (1.0 + e)
+
+
+def test_silu_closed_forms():
+    assert OG.silu(0.0) == 0.0
+    assert OG.silu(1.0) == pytest.approx(1.0 / (1.0 + math.exp(-1.0)), rel=1e-15)
+    assert OG.silu(-1.0) == pytest.approx(-math.exp(-1.0) / (1.0 + math.exp(-1.0)), rel=1e-15)
+    assert OG.silu(60.0) == pytest.approx(60.0, rel=1e-15)             # sigmoid -> 1
+    assert -1e-20 < OG.silu(-60.0) < 0.0                                  # -> 0 from below
+    assert OG.silu(-1e4) == 0.0 and OG.silu(1e4) == 1e4                 # no overflow either way
+
+
+def test_silu_odd_part_is_identity():
+    """silu(g) - silu(-g) = g sigmoid(g) + g (1 - sigmoid(g)) = g for every g."""
+    g = np.random.default_rng(11).standard_normal(1000) * 6
+    np.testing.assert_allclose(OG.silu(g) - OG.silu(-g), g, rtol=1e-14, atol=1e-14)
+
+
+def brute_act(xb, wb):
+    y = brute_force(xb, wb)
+    i = wb.shape[0] // 2
+    return np.array([[silu_math(y[t, f]) * y[t, i + f] for f in range(i)] for t in range(y.shape[0])])
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_act_bruteforce_tiny(seed):
+    T, H, I2 = 3 + seed, 8 + 4 * seed, 2 * (3 + seed)
+    xb, wb = rand_bits(20 + seed, (T, H)), rand_bits(30 + seed, (I2, H), 0.3)
+    np.testing.assert_allclose(OG.gate_up_act(xb, wb), brute_act(xb, wb), rtol=1e-12, atol=1e-15)
+
+
+def test_act_terms_are_the_halves():
+    xb, wb = rand_bits(40, (5, 16)), rand_bits(41, (12, 16), 0.3)
+    z, g, u, ag, au = OG.gate_up_act(xb, wb, with_terms=True)
+    y, a = OG.gate_up(xb, wb, with_abs=True)
+    assert np.array_equal(g, y[:, :6]) and np.array_equal(u, y[:, 6:])
+    assert np.array_equal(ag, a[:, :6]) and np.array_equal(au, a[:, 6:])
+
+
+def test_act_zero_halves():
+    """A zero up half gives zero; a zero gate half gives silu(0) = 0."""
+    xb = rand_bits(42, (4, 16))
+    w = OG.bf16_to_f64(rand_bits(43, (10, 16), 0.3)).astype(np.float32)
+    w_up0, w_gate0 = w.copy(), w.copy()
+    w_up0[5:] = 0.0
+    w_gate0[:5] = 0.0
+    assert not np.any(OG.gate_up_act(xb, bits(w_up0)))
+    assert not np.any(OG.gate_up_act(xb, bits(w_gate0)))
+
+
+def test_act_large_gate_passes_up_through():
+    """With the gate half a large positive multiple of an all-ones row, Z = g u."""
+    H = 8
+    x = np.ones((2, H), np.float32)
+    w = np.zeros((4, H), np.float32)
+    w[:2] = 8.0                                   # g = 64 for every token
+    w[2, 0], w[3, :] = 0.5, -0.25                 # u = 0.5 and -2
+    z = OG.gate_up_act(bits(x), bits(w))
+    np.testing.assert_allclose(z, [[32.0, -128.0], [32.0, -128.0]], rtol=1e-15)
+
+
 # ---------------------------------------------------------------- mutation test
 
 MUTANTS = {
@@ -135,6 +205,10 @@ MUTANTS = {
     "last_feature_dropped": ("Y = X @ W.T", "Y = X[:, :-1] @ W[:, :-1].T"),
     "abs_of_signed_weight": ("np.abs(X) @ np.abs(W).T", "np.abs(X) @ W.T"),
     "rows_from_weight_order": ("Y = X @ W.T", "Y = X @ W[::-1].T"),
+    "silu_sign": ("e = np.exp(-np.abs(g))", "e = np.exp(np.abs(g))"),
+    "act_halves_swapped": ("z = silu(g) * u", "z = silu(u) * g"),
+    "act_without_gate_weight": ("z = silu(g) * u", "z = g * u"),
+    "act_gate_half_shifted": ("g, u = y[:, :i], y[:, i:]", "g, u = y[:, 1:i + 1], y[:, i:]"),
 }
 
 
@@ -159,6 +233,9 @@ def pins_pass(mod) -> bool:
         xb, wb = rand_bits(6, (20, 16)), rand_bits(7, (10, 16))
         rows = np.array([19, 0, 7])
         if not np.allclose(mod.gate_up(xb, wb, rows=rows), brute_force(xb[rows], wb), rtol=1e-13, atol=1e-15):
+            return False
+        xb, wb = rand_bits(8, (3, 12)), rand_bits(9, (8, 12), 0.3)
+        if not np.allclose(mod.gate_up_act(xb, wb), brute_act(xb, wb), rtol=1e-12, atol=1e-15):
             return False
     except Exception:
         return False
