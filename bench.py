@@ -44,6 +44,7 @@ WORKLOADS = {"mixed512": 1, "mbt2048": 2, "mbt16384": 3, "pressure": 4,
              # the fused gate-up projection of the MLP (hidden 2048 -> 2 x 11008) on a chunk
              # of 16,384 or 2,048 tokens, and one 16k prompt as 8 x 2k chunks vs 1 x 16k
              "gateup-16384": ("gateup", 16384), "gateup-2048": ("gateup", 2048), "gateup-chunks": ("gateup", 0),
+             "gateup-act-16384": ("gateup-act", 16384), "gateup-act-2048": ("gateup-act", 2048),
              # request latencies of the paper's bursty trace (seconds-based, steady 0.2 req/s and
              # swept burst rates) under P-PAS and fixed 16k / 2k budgets, every iteration's
              # cost measured on the GPU (one full decoder layer, times 36)
@@ -318,13 +319,15 @@ def run_rope_workload(args, cfg):
     print(json.dumps(rec), flush=True)
 
 
-def run_gateup_workload(args, T):
+def run_gateup_workload(args, T, act=False):
     """ppas_gateup_proj, the MLP's fused gate-up projection Y = X W^T (hidden 2048, 22016
     stacked gate/up rows: the Qwen2.5-3B sizes) on one chunk of T tokens; T = 0 runs one
     16,384-token prompt as eight 2,048-token chunks and as one chunk (Section 6.1,
     Fig. 4b). Weights rotate over four device copies (344 MB, more than the 256 MB
     Infinity Cache), as a layer's weights would be evicted by the other layers' between
-    two of its launches. Kernel time from events recorded by the launch."""
+    two of its launches. Kernel time from events recorded by the launch. With act, the
+    same projection with the gated activation applied in its epilogue (ppas_gateup_act,
+    output [T, 11008]); its FLOP count is the projection's."""
     import numpy as np
     import torch
 
@@ -341,16 +344,18 @@ def run_gateup_workload(args, T):
     w0 = to_device_bf16(wb)
     copies = 4
     ws = [w0] + [w0.clone() for _ in range(copies - 1)]
-    y = torch.empty((Tmax, N), dtype=torch.bfloat16, device="cuda")
+    NO = N // 2 if act else N                     # output columns
+    y = torch.empty((Tmax, NO), dtype=torch.bfloat16, device="cuda")
     hip = HipEvents()
     K = args.steps
 
     wsb = max(ppas.gateup_workspace_bytes(Tmax, H, N), ppas.gateup_workspace_bytes(2048, H, N))
     work = torch.empty(max(wsb, 4), dtype=torch.uint8, device="cuda") if wsb else None
+    call = ppas.gateup_act if act else ppas.gateup_proj
 
     def launch(i, rows=None, ev=None):
         lo, n = (0, Tmax) if rows is None else rows
-        ppas.gateup_proj(x[lo:lo + n], ws[i % copies], y[lo:lo + n], work, ev)
+        call(x[lo:lo + n], ws[i % copies], y[lo:lo + n], work, ev)
 
     def timed(chunks):
         """Median over K rounds of the summed kernel time of the chunks (us each round)."""
@@ -371,18 +376,19 @@ def run_gateup_workload(args, T):
     t_whole = timed(whole)
     us = float(np.median([sum(p) for p in t_whole]))
     F = 2.0 * Tmax * H * N
-    B = 2.0 * (Tmax * H + N * H + Tmax * N)
+    B = 2.0 * (Tmax * H + N * H + Tmax * NO)
     tflops = F / (us * 1e-6) / 1e12
-    wl = f"gateup-{Tmax}x{H}x{N}" if T else f"gateup-prompt16384-8x2048-vs-1x16384-{H}x{N}"
+    name = "gateup-act" if act else "gateup"
+    wl = f"{name}-{Tmax}x{H}x{N}" if T else f"gateup-prompt16384-8x2048-vs-1x16384-{H}x{N}"
     rec = {
         "metric": METRIC, "value": round(tflops, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": round(us * 1e-3, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": wl, "tokens": Tmax, "hidden": H, "gate_up_rows": N,
-                   "weight_copies_rotated": copies},
+                   "weight_copies_rotated": copies, "activation": "silu(gate) * up" if act else None},
         "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(f"gateup-{Tmax}", kernel="gateup_kernel"),
+                     "traffic": measured_traffic(f"{name}-{Tmax}", kernel="gateup_kernel"),
                      "kernel": "gateup_kernel", "kernel_us": round(us, 2),
                      "kernel_us_min": round(min(sum(p) for p in t_whole), 2),
                      "per_launch": {"flop": F, "bytes": B}},
@@ -406,7 +412,10 @@ def run_gateup_workload(args, T):
             while True:
                 rows = np.linspace(0, Tmax - 1, n).astype(np.int64)
                 t0 = time.perf_counter()
-                ref, absv = OG.gate_up(xb, wb, rows=rows, with_abs=True)
+                if act:
+                    ref, gate, up, ag, au = OG.gate_up_act(xb, wb, rows=rows, with_terms=True)
+                else:
+                    ref, absv = OG.gate_up(xb, wb, rows=rows, with_abs=True)
                 dt = time.perf_counter() - t0
                 if dt >= args.cpu_seconds / 4 or n >= Tmax:
                     break
@@ -420,10 +429,17 @@ def run_gateup_workload(args, T):
         torch.cuda.synchronize()
         g = y[torch.from_numpy(rows).cuda()].float().cpu().numpy().astype(np.float64)
         err = np.abs(g - ref)
-        bound = 2.0 ** -8 * np.abs(ref) + (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * absv + 1e-30
+        if act:
+            dg = (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * ag
+            du = (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * au
+            D = 1.1 * dg * (np.abs(up) + du) + np.abs(OG.silu(gate)) * du
+            bound = (2.0 ** -8 * np.abs(ref) + D + 2.0 ** -24 * (np.abs(gate) + 4) * np.abs(ref)) / (1 - 2.0 ** -8)
+            btxt = "(2^-8 |z| + 1.1 d_g (|u| + d_u) + |silu(g)| d_u + 2^-24 (|g| + 4) |z|) / (1 - 2^-8)"
+        else:
+            bound = 2.0 ** -8 * np.abs(ref) + (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * absv
+            btxt = "2^-8 |y| + (1 + 2^-8) 2 H 2^-24 sum_k |x_k w_k| per element"
         rec["parity"] = {"rows": int(len(rows)), "max_abs": float(err.max()), "mean_abs": float(err.mean()),
-                         "max_err_over_bound": float((err / bound).max()),
-                         "bound": "2^-8 |y| + (1 + 2^-8) 2 H 2^-24 sum_k |x_k w_k| per element"}
+                         "max_err_over_bound": float((err / (bound + 1e-30)).max()), "bound": btxt}
     print(json.dumps(rec), flush=True)
 
 
@@ -805,8 +821,8 @@ def main():
         return run_trace_latency_workload(args)
     if args.workload == "serving-sim":
         return run_serving_sim_workload(args)
-    if isinstance(WORKLOADS[args.workload], tuple) and WORKLOADS[args.workload][0] == "gateup":
-        return run_gateup_workload(args, WORKLOADS[args.workload][1])
+    if isinstance(WORKLOADS[args.workload], tuple) and WORKLOADS[args.workload][0] in ("gateup", "gateup-act"):
+        return run_gateup_workload(args, WORKLOADS[args.workload][1], act=WORKLOADS[args.workload][0] == "gateup-act")
     if isinstance(WORKLOADS[args.workload], tuple):
         return run_rope_workload(args, WORKLOADS[args.workload][1])
     rec = measure_step(args, args.workload, not args.no_cpu_baseline)

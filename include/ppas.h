@@ -344,6 +344,31 @@ ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_to
 size_t ppas_gateup_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_out);
 
 /*
+ * The same projection with the MLP's gated activation applied on the way out:
+ * the paper profiles the projection (Section 6.1, Fig. 4b, Table 6); in the
+ * Qwen2.5 models it measures, the MLP then multiplies the SiLU of the gate half
+ * by the up half, and doing that in the projection's epilogue writes half the
+ * bytes and saves a pass over them (the library's own fusion). With n_inter
+ * intermediate features and w [2 n_inter][hidden] (gate rows 0..n_inter-1, then
+ * the up rows of the same features):
+ *   y[t][f] = silu(g) * u,  g = sum_k x[t][k] w[f][k],  u = sum_k x[t][k] w[n_inter + f][k],
+ *   silu(g) = g / (1 + e^-g),  t < n_tokens, f < n_inter
+ * y [n_tokens][n_inter] bf16; g and u are accumulated in fp32 as in
+ * ppas_gateup_proj, silu(g) * u is evaluated in fp32 and rounded to bf16
+ * nearest-even. Workspace, splits, events, streams and status codes as for
+ * ppas_gateup_proj with n_out = 2 n_inter; n_inter above (2^31 - 513) / 2 is
+ * PPAS_ERANGE.
+ */
+ppas_status ppas_gateup_act(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden,
+                            int32_t n_inter, void* workspace, size_t workspace_bytes,
+                            const ppas_events* events, void* hip_stream);
+
+/* Workspace ppas_gateup_act uses for this shape on the current device (0 when it
+ * does not split the reduction, or for an invalid shape). The library's own
+ * sizing call. */
+size_t ppas_gateup_act_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_inter);
+
+/*
  * For callers that cannot allocate memory: code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc. Computes exactly what
  * ppas_attn_step computes, with the same plan and kernels (bit-identical

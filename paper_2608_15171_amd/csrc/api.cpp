@@ -492,26 +492,58 @@ size_t ppas_gateup_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_o
   }
 }
 
+namespace {
+
+// Both projection entry points: n_out weight rows; with `act` the output holds the
+// gated activation of the two halves (n_out / 2 columns).
+ppas_status gateup_call(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_out,
+                        bool act, void* workspace, size_t workspace_bytes, const ppas_events* events,
+                        void* hip_stream) {
+  ppas_status st = check_gateup(n_tokens, hidden, n_out);
+  if (st != PPAS_OK) return st;
+  st = check_events(events);
+  if (st != PPAS_OK) return st;
+  if (n_tokens == 0) return PPAS_OK;
+  if (!x || !w || !y || (workspace_bytes > 0 && !workspace)) return PPAS_EINVAL;
+  const DeviceInfo dev = current_device();
+  if (!dev.gfx950) return PPAS_EUNSUPPORTED;
+  // the automatic split, reduced to what the workspace holds (no split needs none)
+  int splits = gateup_splits(n_tokens, hidden, n_out, dev.cus);
+  while (splits > 1 && gateup_workspace_bytes(n_tokens, n_out, splits) > workspace_bytes) --splits;
+  if (gateup_tiles(n_tokens, n_out) * splits > INT32_MAX) splits = 1;
+  const hipError_t e = launch_gateup(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
+                                     static_cast<uint16_t*>(y), n_tokens, hidden, n_out, act, splits,
+                                     static_cast<float*>(workspace), dev.cus, static_cast<hipStream_t>(hip_stream),
+                                     ev_of(events, 0), ev_of(events, 1));
+  return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
+}
+
+// weight rows of the activated projection (two per intermediate feature), or -1
+int32_t act_rows(int32_t n_inter) { return (n_inter <= 0 || n_inter > (INT32_MAX - 512) / 2) ? -1 : 2 * n_inter; }
+
+}  // namespace
+
 ppas_status ppas_gateup_proj(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_out,
                              void* workspace, size_t workspace_bytes, const ppas_events* events, void* hip_stream) {
   try {
-    ppas_status st = check_gateup(n_tokens, hidden, n_out);
-    if (st != PPAS_OK) return st;
-    st = check_events(events);
-    if (st != PPAS_OK) return st;
-    if (n_tokens == 0) return PPAS_OK;
-    if (!x || !w || !y || (workspace_bytes > 0 && !workspace)) return PPAS_EINVAL;
-    const DeviceInfo dev = current_device();
-    if (!dev.gfx950) return PPAS_EUNSUPPORTED;
-    // the automatic split, reduced to what the workspace holds (no split needs none)
-    int splits = gateup_splits(n_tokens, hidden, n_out, dev.cus);
-    while (splits > 1 && gateup_workspace_bytes(n_tokens, n_out, splits) > workspace_bytes) --splits;
-    if (gateup_tiles(n_tokens, n_out) * splits > INT32_MAX) splits = 1;
-    const hipError_t e = launch_gateup(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
-                                       static_cast<uint16_t*>(y), n_tokens, hidden, n_out, splits,
-                                       static_cast<float*>(workspace), dev.cus, static_cast<hipStream_t>(hip_stream),
-                                       ev_of(events, 0), ev_of(events, 1));
-    return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
+    return gateup_call(x, w, y, n_tokens, hidden, n_out, false, workspace, workspace_bytes, events, hip_stream);
+  } catch (...) {
+    return PPAS_EINVAL;
+  }
+}
+
+size_t ppas_gateup_act_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_inter) {
+  const int32_t n_out = act_rows(n_inter);
+  return n_out < 0 ? 0 : ppas_gateup_workspace_bytes(n_tokens, hidden, n_out);
+}
+
+ppas_status ppas_gateup_act(const void* x, const void* w, void* y, int32_t n_tokens, int32_t hidden, int32_t n_inter,
+                            void* workspace, size_t workspace_bytes, const ppas_events* events, void* hip_stream) {
+  try {
+    if (n_inter > (INT32_MAX - 512) / 2) return PPAS_ERANGE;
+    const int32_t n_out = act_rows(n_inter);
+    if (n_out < 0) return PPAS_EINVAL;
+    return gateup_call(x, w, y, n_tokens, hidden, n_out, true, workspace, workspace_bytes, events, hip_stream);
   } catch (...) {
     return PPAS_EINVAL;
   }

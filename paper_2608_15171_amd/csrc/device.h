@@ -28,12 +28,14 @@ hipError_t launch_attn_step(const uint16_t* q, uint16_t* out, const uint16_t* kp
                             hipEvent_t ev_start, hipEvent_t ev_stop, hipEvent_t ev_merge_start,
                             hipEvent_t ev_merge_stop);
 
-// The gate-up projection: y = x w^T (hidden a multiple of 64). With splits > 1
-// the reduction is split over that many workgroups per output tile, whose fp32
-// partial sums (gateup_workspace_bytes of `part`) a second launch adds in order.
-// `cus` is the device's compute-unit count (the grid holds one workgroup per unit).
+// The gate-up projection: y = x w^T (hidden a multiple of 64), or with `act` the
+// gated activation of its two halves, y[t][f] = silu(s[t][f]) s[t][N2/2 + f]
+// (N2 even, y [T][N2/2]). With splits > 1 the reduction is split over that many
+// workgroups per output tile, whose fp32 partial sums (gateup_workspace_bytes of
+// `part`, columns in weight-row order) a second launch adds in order. `cus` is
+// the device's compute-unit count (the grid holds one workgroup per unit).
 hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t T, int32_t H, int32_t N2,
-                         int splits, float* part, int cus, hipStream_t stream, hipEvent_t ev_start,
+                         bool act, int splits, float* part, int cus, hipStream_t stream, hipEvent_t ev_start,
                          hipEvent_t ev_stop);
 // Output tiles of a call: 256 x 256, plus 64 x 256 for the last T % 256 token rows.
 int64_t gateup_tiles(int32_t T, int32_t N2);

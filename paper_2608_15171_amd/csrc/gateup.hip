@@ -105,6 +105,7 @@ struct GemmArgs {
   int32_t tiles_m, tiles_n;   // full 256-row tiles, 256-column tiles
   int32_t tail_m;             // 64-row tiles of the last T % 256 rows
   int32_t splits;             // reduction split over this many workgroups per tile
+  int32_t I;                  // with the gated activation: N2 / 2 intermediate features
 };
 
 __device__ __forceinline__ u32x4 lds16(const char* p) { return *reinterpret_cast<const u32x4*>(p); }
@@ -120,6 +121,12 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   const f32x2 v = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// silu(g) = g / (1 + e^-g) in fp32 (e^-g through the hardware base-2 exponential;
+// +inf for large negative g, which gives -0).
+__device__ __forceinline__ float silu_f32(float g) {
+  return g / (1.f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f));
 }
 
 // 16 bytes from global memory into LDS: lane L of the wave lands at lds + 16 L.
@@ -170,7 +177,7 @@ __device__ __forceinline__ void bare_barrier() {
 //   eight waves: 128 x 64 (full),   64 x 32 (tail)
 // The W part of a stage is always 256 rows, the X part BM rows; the first half
 // of the waves copy the W part, the second half the X part, in equal shares.
-template <int BM>
+template <int BM, bool kAct>
 __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0, int n0, int split, int k_lo,
                                           int k_hi) {
   constexpr int WN = (BM == kBM || kWaves == 4) ? 128 : 64;   // columns per wave
@@ -202,7 +209,15 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
     for (int i = 0; i < kDmaMax; ++i) {
       const int R = rows_half * half + i * kRowsPerDma + lane / kCPR;   // row within the part
       const int c = (lane % kCPR) ^ swizzle(R);
-      const int r = min(r0 + i * kRowsPerDma + lane / kCPR, rmax);     // rows past the edge read the last row
+      int r = min(r0 + i * kRowsPerDma + lane / kCPR, rmax);           // rows past the edge read the last row
+      if (kAct && !is_x) {
+        // with the gated activation the tile covers features n0 / 2 .. + 127: the
+        // rows of wave column group R / WN are gate rows of WN / 2 features, then
+        // the up rows of the same features (features past the end read the last)
+        const int rr = R % WN;
+        const int f = min(n0 / 2 + (WN / 2) * (R / WN) + rr % (WN / 2), a.I - 1);
+        r = rr < WN / 2 ? f : a.I + f;
+      }
       gptr[i] = base + size_t(r) * a.H + 8 * c;
     }
   }
@@ -356,18 +371,88 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
         if (m >= a.T) continue;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int n = nw + 32 * ti + 8 * g + 4 * (lane >> 5);
+          // columns n .. n + 3, valid below `lim`
+          int n = nw + 32 * ti + 8 * g + 4 * (lane >> 5);
+          int lim = a.N2;
+          bool vec = (a.N2 & 3) == 0;
+          if (kAct) {
+            // partials keep the weight-row order: gate feature f at column f,
+            // its up row at I + f (features from I on belong to neither)
+            const int f = n0 / 2 + (WN / 2) * wn + 32 * (ti % (kNT / 2)) + 8 * g + 4 * (lane >> 5);
+            if (f >= a.I) continue;
+            n = ti < kNT / 2 ? f : a.I + f;
+            lim = ti < kNT / 2 ? a.I : a.N2;
+            vec = (a.I & 3) == 0;
+          }
           float* dst = pb + size_t(m) * a.N2 + n;
-          if (n + 4 <= a.N2 && (a.N2 & 3) == 0) {
+          if (n + 4 <= lim && vec) {
             *reinterpret_cast<f32x4*>(dst) =
                 f32x4{acc[ti][tj][4 * g], acc[ti][tj][4 * g + 1], acc[ti][tj][4 * g + 2], acc[ti][tj][4 * g + 3]};
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
-              if (n + e < a.N2) dst[e] = acc[ti][tj][4 * g + e];
+              if (n + e < lim) dst[e] = acc[ti][tj][4 * g + e];
           }
         }
       }
+    return;
+  }
+
+  if constexpr (kAct) {
+    // silu(gate) * up: MFMA tiles ti and ti + kNT / 2 hold the gate and the up
+    // value of the same (token row, feature) in the same register; the wave's
+    // WN / 2 features x WM rows go to LDS, then out in WN-byte row runs.
+    char* eb = smem + w * kEpiWave;
+#pragma unroll
+    for (int ti = 0; ti < kNT / 2; ++ti)
+#pragma unroll
+      for (int tj = 0; tj < kMT; ++tj)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int row = 32 * tj + (lane & 31);
+          const int col = 32 * ti + 8 * g + 4 * (lane >> 5);
+          float z[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[e] = silu_f32(acc[ti][tj][4 * g + e]) * acc[ti + kNT / 2][tj][4 * g + e];
+          u32x2 v;
+          v[0] = pack_bf16x2(z[0], z[1]);
+          v[1] = pack_bf16x2(z[2], z[3]);
+          *reinterpret_cast<u32x2*>(eb + row * kPitch + col * 2) = v;
+        }
+    __syncthreads();
+    constexpr int WF = WN / 2;                       // features per wave
+    constexpr int kLPR = WF / 8, kRPI = 64 / kLPR, kIters = WM / kRPI;
+    const int fw = n0 / 2 + WF * wn;
+    const int fb = fw + 8 * (lane % kLPR);
+    if (mw + WM <= a.T && fw + WF <= a.I) {
+      constexpr int kB = kIters < 8 ? kIters : 8;
+#pragma unroll
+      for (int s0 = 0; s0 < kIters; s0 += kB) {
+        u32x4 v[kB];
+#pragma unroll
+        for (int i = 0; i < kB; ++i)
+          v[i] = lds16(eb + (kRPI * (s0 + i) + lane / kLPR) * kPitch + 16 * (lane % kLPR));
+#pragma unroll
+        for (int i = 0; i < kB; ++i)
+          *reinterpret_cast<u32x4*>(a.y + size_t(mw + kRPI * (s0 + i) + lane / kLPR) * a.I + fb) = v[i];
+      }
+      return;
+    }
+#pragma unroll 4
+    for (int s = 0; s < kIters; ++s) {
+      const int row = kRPI * s + lane / kLPR;
+      const int m = mw + row;
+      if (m >= a.T) break;
+      const u32x4 v = lds16(eb + row * kPitch + 16 * (lane % kLPR));
+      uint16_t* dst = a.y + size_t(m) * a.I + fb;
+      if (fb + 8 <= a.I) {
+        *reinterpret_cast<u32x4*>(dst) = v;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (fb + e < a.I) dst[e] = uint16_t(v[e >> 1] >> (16 * (e & 1)));
+      }
+    }
     return;
   }
 
@@ -422,6 +507,7 @@ __device__ __forceinline__ void tile_body(const GemmArgs& a, char* smem, int m0,
   }
 }
 
+template <bool kAct>
 __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem[kSmem];
 
@@ -449,11 +535,11 @@ __global__ __launch_bounds__(kThreads, 1) void gateup_kernel(GemmArgs a) {
       const int first_m = grp * kGroupM;
       const int gm = min(kGroupM, a.tiles_m - first_m);
       const int in_grp = t - grp * kGroupM * a.tiles_n;
-      tile_body<kBM>(a, smem, (first_m + in_grp % gm) * kBM, (in_grp / gm) * kBN, split, k_lo, k_hi);
+      tile_body<kBM, kAct>(a, smem, (first_m + in_grp % gm) * kBM, (in_grp / gm) * kBN, split, k_lo, k_hi);
     } else {
       const int tt = t - full;
-      tile_body<kBMTail>(a, smem, a.tiles_m * kBM + (tt % a.tail_m) * kBMTail, (tt / a.tail_m) * kBN, split,
-                         k_lo, k_hi);
+      tile_body<kBMTail, kAct>(a, smem, a.tiles_m * kBM + (tt % a.tail_m) * kBMTail, (tt / a.tail_m) * kBN,
+                               split, k_lo, k_hi);
     }
     // the next item's transfers overwrite the LDS this item's epilogue has read;
     // its stores may still be in flight
@@ -484,6 +570,42 @@ __global__ __launch_bounds__(256) void gateup_reduce_kernel(const float* part, u
   }
 }
 
+// The gated activation from split partials: z[m][f] = bf16(silu(g) * u), g and u
+// the in-order sums over splits of partial columns f and I + f of row m. Thread i
+// covers elements 4i .. 4i + 3 of the flattened [T][I] output.
+__global__ __launch_bounds__(256) void gateup_act_reduce_kernel(const float* part, uint16_t* y, int32_t T,
+                                                                int32_t I, int32_t splits) {
+  const int64_t total = int64_t(T) * I;
+  const int64_t e0 = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (e0 >= total) return;
+  const int64_t plane = int64_t(T) * 2 * I;   // one split's [T][2I] partials
+  auto one = [&](int64_t e) {
+    const int64_t m = e / I, f = e % I;
+    const float* pg = part + m * 2 * I + f;
+    float g = pg[0], u = pg[I];
+    for (int k = 1; k < splits; ++k) {
+      g += pg[size_t(k) * plane];
+      u += pg[size_t(k) * plane + I];
+    }
+    return silu_f32(g) * u;
+  };
+  if ((I & 3) == 0 && e0 + 4 <= total) {
+    const int64_t m = e0 / I, f = e0 % I;
+    const float* pg = part + m * 2 * I + f;
+    f32x4 g = *reinterpret_cast<const f32x4*>(pg), u = *reinterpret_cast<const f32x4*>(pg + I);
+    for (int k = 1; k < splits; ++k) {
+      g += *reinterpret_cast<const f32x4*>(pg + size_t(k) * plane);
+      u += *reinterpret_cast<const f32x4*>(pg + size_t(k) * plane + I);
+    }
+    u32x2 v;
+    v[0] = pack_bf16x2(silu_f32(g[0]) * u[0], silu_f32(g[1]) * u[1]);
+    v[1] = pack_bf16x2(silu_f32(g[2]) * u[2], silu_f32(g[3]) * u[3]);
+    *reinterpret_cast<u32x2*>(y + e0) = v;
+  } else {
+    for (int64_t e = e0; e < e0 + 4 && e < total; ++e) y[e] = uint16_t(pack_bf16x2(one(e), 0.f) & 0xffff);
+  }
+}
+
 }  // namespace
 
 int64_t gateup_tiles(int32_t T, int32_t N2) {
@@ -503,7 +625,7 @@ size_t gateup_workspace_bytes(int32_t T, int32_t N2, int splits) {
 }
 
 hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t T, int32_t H, int32_t N2,
-                         int splits, float* part, int cus, hipStream_t stream, hipEvent_t ev_start,
+                         bool act, int splits, float* part, int cus, hipStream_t stream, hipEvent_t ev_start,
                          hipEvent_t ev_stop) {
   GemmArgs a;
   a.x = x;
@@ -517,22 +639,32 @@ hipError_t launch_gateup(const uint16_t* x, const uint16_t* w, uint16_t* y, int3
   a.tail_m = (T % kBM + kBMTail - 1) / kBMTail;
   a.tiles_n = (N2 + kBN - 1) / kBN;
   a.splits = splits;
+  a.I = N2 / 2;
   const int64_t n = gateup_tiles(T, N2) * splits;
   if (n <= 0) return hipSuccess;
-  if (n > INT32_MAX || splits < 1 || splits > H / kBK || (splits > 1 && !part)) return hipErrorInvalidValue;
+  if (n > INT32_MAX || splits < 1 || splits > H / kBK || (splits > 1 && !part) || (act && N2 % 2 != 0))
+    return hipErrorInvalidValue;
   // one workgroup per compute unit, each looping over its items (a multiple of 8
   // workgroups, so that every workgroup stays on one XCD's share of the items)
   const int64_t slots = kPersist ? std::max(8, cus / 8 * 8) : n;
   const int64_t grid = std::min<int64_t>(n, slots);
-  hipExtLaunchKernelGGL(gateup_kernel, dim3(unsigned(grid)), dim3(kThreads), 0, stream, ev_start,
-                        splits > 1 ? nullptr : ev_stop, 0, a);
+  if (act)
+    hipExtLaunchKernelGGL(gateup_kernel<true>, dim3(unsigned(grid)), dim3(kThreads), 0, stream, ev_start,
+                          splits > 1 ? nullptr : ev_stop, 0, a);
+  else
+    hipExtLaunchKernelGGL(gateup_kernel<false>, dim3(unsigned(grid)), dim3(kThreads), 0, stream, ev_start,
+                          splits > 1 ? nullptr : ev_stop, 0, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
-  const int64_t total = int64_t(T) * N2;
+  const int64_t total = act ? int64_t(T) * (N2 / 2) : int64_t(T) * N2;
   const int64_t blocks = (total + 1023) / 1024;
   if (blocks > INT32_MAX) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL(gateup_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, nullptr, ev_stop, 0,
-                        static_cast<const float*>(part), y, total, splits);
+  if (act)
+    hipExtLaunchKernelGGL(gateup_act_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, nullptr, ev_stop,
+                          0, static_cast<const float*>(part), y, T, N2 / 2, splits);
+  else
+    hipExtLaunchKernelGGL(gateup_reduce_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, nullptr, ev_stop, 0,
+                          static_cast<const float*>(part), y, total, splits);
   return hipGetLastError();
 }
 

@@ -7,11 +7,12 @@ A layer here is the work the paper's profiling names for a prefill chunk and its
 neighbours in the block (Section 6.1): the projections of the attention input
 (Q, K and V in one GEMM), the rotary embedding fused with the page write of the
 new keys and values, the packed attention over the paged cache (with its split
-merge), the output projection, the fused gate-up projection and the down
-projection. All four projections run on the library's MFMA GEMM
-(ppas_gateup_proj computes any y = x w^T with a hidden size that is a multiple
-of 64, splitting the reduction across workgroups when the output has few tiles,
-as the decode-sized and 2k-sized projections do). Left out: the two RMS norms, the SiLU-and-multiply and the residual adds
+merge), the output projection, the fused gate-up projection with the MLP's gated
+SiLU activation in its epilogue (ppas_gateup_act), and the down projection of its
+output. All four projections run on the library's MFMA GEMM (ppas_gateup_proj
+computes any y = x w^T with a hidden size that is a multiple of 64, splitting the
+reduction across workgroups when the output has few tiles, as the decode-sized
+and 2k-sized projections do). Left out: the two RMS norms and the residual adds
 (elementwise, a few per cent of a prefill iteration at their HBM roofline) and
 the once-per-iteration embedding, LM head and sampling.
 
@@ -66,12 +67,11 @@ class DecoderLayerCost:
         self.kn = rand(T, Hkv, D)
         self.vn = rand(T, Hkv, D)
         self.x = rand(T, H)
-        self.xi = rand(T, cfg["inter"])
         self.attn_out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=device)
         qkv_rows = (Hq + 2 * Hkv) * D
         self.y = {"qkv": torch.empty((T, qkv_rows), dtype=torch.bfloat16, device=device),
                   "o": torch.empty((T, H), dtype=torch.bfloat16, device=device),
-                  "gate_up": torch.empty((T, 2 * cfg["inter"]), dtype=torch.bfloat16, device=device),
+                  "gate_up": torch.empty((T, cfg["inter"]), dtype=torch.bfloat16, device=device),
                   "down": torch.empty((T, H), dtype=torch.bfloat16, device=device)}
         self.w = [{"qkv": rand(qkv_rows, H, scale=0.02), "o": rand(H, Hq * D, scale=0.02),
                    "gate_up": rand(2 * cfg["inter"], H, scale=0.02), "down": rand(H, cfg["inter"], scale=0.02)}
@@ -104,7 +104,7 @@ class DecoderLayerCost:
         H, I2 = self.cfg["hidden"], self.cfg["inter"]
         need = max(ppas.gateup_workspace_bytes(T, H, self.y["qkv"].shape[1]),
                    ppas.gateup_workspace_bytes(T, self.cfg["q_heads"] * self.cfg["head_dim"], H),
-                   ppas.gateup_workspace_bytes(T, H, 2 * I2), ppas.gateup_workspace_bytes(T, I2, H))
+                   ppas.gateup_act_workspace_bytes(T, H, I2), ppas.gateup_workspace_bytes(T, I2, H))
         if self.gws.numel() < need:
             self.gws = torch.empty(need, dtype=torch.uint8, device=self.device)
         gws = self.gws
@@ -115,8 +115,8 @@ class DecoderLayerCost:
         plan.attn_step(self.attn_out[:T], self.q[:T], self.kp, self.vp, bt, self.ws,
                        ppas.events(e[4], e[5], *((e[6], e[7]) if merge else (None, None))))
         ppas.gateup_proj(self.attn_out[:T].view(T, -1), w["o"], self.y["o"][:T], gws, ppas.events(e[8], e[9]))
-        ppas.gateup_proj(self.x[:T], w["gate_up"], self.y["gate_up"][:T], gws, ppas.events(e[10], e[11]))
-        ppas.gateup_proj(self.xi[:T], w["down"], self.y["down"][:T], gws, ppas.events(e[12], e[13]))
+        ppas.gateup_act(self.x[:T], w["gate_up"], self.y["gate_up"][:T], gws, ppas.events(e[10], e[11]))
+        ppas.gateup_proj(self.y["gate_up"][:T], w["down"], self.y["down"][:T], gws, ppas.events(e[12], e[13]))
         torch.cuda.synchronize()
         plan.close()
         el = self.hip.elapsed_ms

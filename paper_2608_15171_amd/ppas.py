@@ -95,6 +95,10 @@ _lib.ppas_gateup_proj.restype = ctypes.c_int
 _lib.ppas_gateup_proj.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _sz, _E, _vp]
 _lib.ppas_gateup_workspace_bytes.restype = _sz
 _lib.ppas_gateup_workspace_bytes.argtypes = [_i32, _i32, _i32]
+_lib.ppas_gateup_act.restype = ctypes.c_int
+_lib.ppas_gateup_act.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _sz, _E, _vp]
+_lib.ppas_gateup_act_workspace_bytes.restype = _sz
+_lib.ppas_gateup_act_workspace_bytes.argtypes = [_i32, _i32, _i32]
 _lib.ppas_plan_items.restype = _i32
 _lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
 _lib.ppas_step_plan_create.restype = ctypes.c_int
@@ -282,6 +286,29 @@ def gateup_proj(x, w, y, workspace=None, events: Events | None = None, stream=No
     st = _lib.ppas_gateup_proj(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N, _dev(workspace, "workspace"),
                                ws_bytes, None if events is None else ctypes.byref(events), _stream(stream))
     _check(st, "ppas_gateup_proj")
+
+
+def gateup_act_workspace_bytes(n_tokens: int, hidden: int, n_inter: int) -> int:
+    return int(_lib.ppas_gateup_act_workspace_bytes(int(n_tokens), int(hidden), int(n_inter)))
+
+
+def gateup_act(x, w, y, workspace=None, events: Events | None = None, stream=None) -> None:
+    """y = silu(x w_gate^T) * (x w_up^T): the gate-up projection with the gated activation
+    (x [T, H], w [2I, H] with the gate rows over the up rows, y [T, I], bf16 device tensors).
+    workspace: a device buffer for split reductions (see gateup_act_workspace_bytes), or None."""
+    for t, name in ((x, "x"), (w, "w"), (y, "y")):
+        if t.dim() != 2 or t.element_size() != 2:
+            raise ValueError(f"{name} must be a 2-D bf16 tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    T, H = x.shape
+    N = w.shape[0]
+    if N % 2 or w.shape[1] != H or tuple(y.shape) != (T, N // 2):
+        raise ValueError(f"shapes x {tuple(x.shape)}, w {tuple(w.shape)}, y {tuple(y.shape)} do not match")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.ppas_gateup_act(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N // 2, _dev(workspace, "workspace"),
+                              ws_bytes, None if events is None else ctypes.byref(events), _stream(stream))
+    _check(st, "ppas_gateup_act")
 
 
 def plan_opts(prefill_split: int = 0, decode_split: int = 0, tile_positions: int = 0, num_cus: int = 0) -> PlanOpts:

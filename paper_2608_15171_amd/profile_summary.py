@@ -42,10 +42,19 @@ DESCRIPTION = {
     "gateup_kernel": "The MLP's fused gate-up projection Y = X W^T (hidden 2048, 22016 stacked gate/up rows), one "
                      "launch on one MI355X (gfx950); bf16 inputs, fp32 accumulation.",
 }
+DESCRIPTION_ACT = ("The MLP's gate-up projection with the gated activation in its epilogue, Z = silu(X W_gate^T) * "
+                   "(X W_up^T) (hidden 2048, 11008 features), one launch on one MI355X (gfx950); bf16 inputs, fp32 "
+                   "accumulation and activation.")
+
+
+def describe(kernel: str, workload: str) -> str:
+    return DESCRIPTION_ACT if workload.startswith("gateup-act") else DESCRIPTION[kernel]
+
+
 ALGORITHMIC = {
     "attn_step_kernel": "algorithmic bytes (visible K/V once + Q + O)",
     "rope_append_kernel": "algorithmic bytes (Q read and written, new K/V read and written, once each)",
-    "gateup_kernel": "algorithmic bytes (X and W read once, Y written once)",
+    "gateup_kernel": "algorithmic bytes (X and W read once, the output written once)",
 }
 
 
@@ -97,7 +106,7 @@ def main(workload: str, d: str, calib: str, kernel: str = "attn_step_kernel"):
     json.dump(rec, open(out + ".traffic.json", "w"), indent=1)
     cmd = f"bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline"
     lines = [f"# {kernel} -- workload {wl_name} ({workload})", "",
-             DESCRIPTION[kernel], "",
+             describe(kernel, workload), "",
              "## Kernel trace (rocprofv3 --kernel-trace --stats)", "", "Command:", "",
              f"    cd /tmp && TMPDIR=/tmp rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- "
              f"python3 <repo>/{cmd}", "",
@@ -163,7 +172,7 @@ def mfma_summary(workload: str, d: str, kernel: str = "", simds: int = 1024, xcd
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d <out> -o run "
            f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
     lines = [f"# {kernel} -- matrix-core utilisation, workload {bench['config']['workload']} ({workload})", "",
-             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
              f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
              f"| engine clock | {clock:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",
@@ -209,7 +218,7 @@ def stall_summary(workload: str, d: str, kernel: str = "", cus: int = 256, xcds:
            f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
     share = lambda k: f"{100 * m[k] / wave:.1f} % of wave time"
     lines = [f"# {kernel} -- where the waves spend their time, workload {bench['config']['workload']} ({workload})", "",
-             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
              f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
              f"| engine clock | {cycles / us / 1e3:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",
@@ -249,7 +258,7 @@ def cache_summary(workload: str, d: str, kernel: str = "gateup_kernel", xcds: in
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(CACHE_COUNTERS)} --output-format csv -d <out> -o run "
            f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
     lines = [f"# {kernel} -- L2 hit rate, workload {bench['config']['workload']} ({workload})", "",
-             DESCRIPTION[kernel], "", "Command (one counter pass):", "", "    " + cmd, "",
+             describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
              f"| kernel time under the profiler | {us:.1f} us | dispatch timestamps, mean of the pass's last two launches |",
              f"| engine clock | {m['GRBM_GUI_ACTIVE'] / xcds / us / 1e3:.2f} GHz | GRBM_GUI_ACTIVE / {xcds} XCDs / kernel time |",

@@ -189,6 +189,29 @@ def test_gateup_workspace_sizing():
     assert W(0, 2048, 2048) == 0 and W(4, 96, 8) == 0
 
 
+def test_gateup_act_validates_before_any_device_work():
+    f = ppas._lib.ppas_gateup_act
+    assert f(1, 1, 1, 0, 64, 4, None, 0, None, None) == ppas.PPAS_OK                 # no tokens: nothing to do
+    assert f(1, 1, 1, 4, 96, 4, None, 0, None, None) == ppas.PPAS_EUNSUPPORTED       # hidden not a multiple of 64
+    assert f(1, 1, 1, -1, 64, 4, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 64, 0, None, 0, None, None) == ppas.PPAS_EINVAL            # no intermediate features
+    assert f(1, 1, 1, 4, 64, -3, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, None, 4, 64, 4, None, 0, None, None) == ppas.PPAS_EINVAL
+    assert f(1, 1, 1, 4, 64, 2 ** 30, None, 0, None, None) == ppas.PPAS_ERANGE     # 2 n_inter weight rows overflow
+    assert f(1, 1, 1, 4, 64, 4, None, 1024, None, None) == ppas.PPAS_EINVAL
+    half = ppas.events(stop=1)
+    assert f(1, 1, 1, 4, 64, 4, None, 0, ctypes.byref(half), None) == ppas.PPAS_EINVAL
+
+
+def test_gateup_act_workspace_is_the_projection_s():
+    """The activated projection splits like the projection of its 2 n_inter weight rows
+    (its partials keep the weight-row layout)."""
+    for T, H, I in ((16, 2048, 11008), (2048, 2048, 11008), (16, 2048, 1024), (300, 128, 40)):
+        assert ppas.gateup_act_workspace_bytes(T, H, I) == ppas.gateup_workspace_bytes(T, H, 2 * I)
+    assert ppas.gateup_act_workspace_bytes(16, 2048, 0) == 0
+    assert ppas.gateup_act_workspace_bytes(16, 2048, 2 ** 30) == 0
+
+
 def check_coverage(spec, items):
     """Every (row, query head) sees keys 0..p split over items without gaps or overlaps,
     and each item gives each of its rows at least one visible key."""

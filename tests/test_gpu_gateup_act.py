@@ -1,0 +1,129 @@
+"""GPU parity of the gate-up projection with the gated activation (ppas_gateup_act)
+against the fp64 oracle (oracle.gemm.gate_up_act), through the C ABI.
+
+Bound per output element, derived from the kernel's arithmetic. The gate and up
+sums g~ and u~ carry the projection's accumulation error, at most
+d_g = (1 + 2^-8) 2 H 2^-24 A_g (A_g = sum_k |x_k w_k| over the gate row; d_u the
+same over the up row), and are not rounded before the activation. silu has slope
+at most 1.1 in magnitude, so
+    |silu(g~) u~ - silu(g) u| <= 1.1 d_g (|u| + d_u) + |silu(g)| d_u = D.
+The fp32 evaluation of silu(g~) u~ (the exponential of a rounded argument, one
+division, one product) adds at most 2^-24 (|g| + 4) |silu(g) u|, and the final
+rounding to bf16 nearest at most 2^-8 of the stored value, so
+    |gpu - z| <= (2^-8 |z| + D + 2^-24 (|g| + 4) |z|) / (1 - 2^-8).
+Ragged shapes (token rows not multiples of 256, features not multiples of the
+128 a tile covers, split and unsplit reductions) are compared on every element;
+the Qwen2.5-3B sizes (hidden 2048, 11008 features) on sampled rows, every feature.
+"""
+import numpy as np
+import pytest
+
+import oracle.gemm as OG
+from paper_2608_15171_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_15171_amd import ppas, step
+    return ppas, step, torch
+
+
+def run(lib, xb, wb, split=True):
+    ppas, step, torch = lib
+    x = step.to_device_bf16(xb)
+    w = step.to_device_bf16(wb)
+    n_inter = wb.shape[0] // 2
+    y = torch.full((xb.shape[0], n_inter), float("nan"), dtype=torch.bfloat16, device="cuda")
+    n = ppas.gateup_act_workspace_bytes(xb.shape[0], xb.shape[1], n_inter) if split else 0
+    ws = torch.full((max(n // 4, 1),), float("nan"), dtype=torch.float32, device="cuda") if n else None
+    ppas.gateup_act(x, w, y, ws)
+    torch.cuda.synchronize()
+    return y
+
+
+def f64(y):
+    return y.float().cpu().numpy().astype(np.float64)
+
+
+def check(g, xb, wb, rows=None, label=""):
+    z, gate, up, ag, au = OG.gate_up_act(xb, wb, rows=rows, with_terms=True)
+    assert np.isfinite(g).all(), f"{label}: non-finite output"
+    H = xb.shape[1]
+    dg = (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * ag
+    du = (1 + 2.0 ** -8) * 2 * H * 2.0 ** -24 * au
+    D = 1.1 * dg * (np.abs(up) + du) + np.abs(OG.silu(gate)) * du
+    bound = (2.0 ** -8 * np.abs(z) + D + 2.0 ** -24 * (np.abs(gate) + 4) * np.abs(z)) / (1 - 2.0 ** -8) + 1e-30
+    err = np.abs(g - z)
+    worst = float((err / bound).max())
+    print(f"{label}: max_abs={err.max():.3e} err/bound={worst:.3f}", flush=True)
+    assert worst <= 1.0, f"{label}: {int((err > bound).sum())} elements beyond the bound"
+
+
+@pytest.mark.parametrize("T,H,NI", [(1, 64, 1), (5, 64, 150), (31, 128, 17), (257, 128, 256), (300, 192, 260),
+                                    (256, 256, 128), (513, 2048, 300), (700, 640, 515),
+                                    # split reductions: decode-sized and small-chunk calls
+                                    (16, 2048, 11008), (3, 2048, 1025), (100, 2048, 1280), (2048, 2048, 1024)])
+@pytest.mark.parametrize("split", [True, False])
+def test_ragged_shapes_every_element(lib, T, H, NI, split):
+    ppas = lib[0]
+    print(f"gate-up-act T={T} H={H} I={NI} split={split} workspace={ppas.gateup_act_workspace_bytes(T, H, NI)}",
+          flush=True)
+    xb = I.gateup_tokens(3, T, 0, hidden=H)
+    wb = I.gateup_weight(3, hidden=H, inter=NI)
+    check(f64(run(lib, xb, wb, split)), xb, wb, label=f"T{T} H{H} I{NI} split={split}")
+
+
+def test_split_reduction_is_deterministic(lib):
+    torch = lib[2]
+    xb = I.gateup_tokens(4, 40, 0, hidden=2048)
+    wb = I.gateup_weight(4, hidden=2048, inter=2048)
+    a, b = run(lib, xb, wb), run(lib, xb, wb)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def sample_rows(T):
+    edges = [0, 1, 31, 32, 63, 64, 255, 256, 257, T - 257, T - 256, T - 1]
+    mid = np.random.default_rng(T + 1).integers(0, T, 40)
+    return np.unique(np.clip(np.r_[edges, mid], 0, T - 1))
+
+
+@pytest.mark.parametrize("T", [2048, 16384])
+def test_qwen25_3b_sizes_sampled_rows(lib, T):
+    print(f"gate-up-act T={T} H={I.GATEUP_HIDDEN} I={I.GATEUP_INTER}", flush=True)
+    xb = I.gateup_tokens(0, T)
+    wb = I.gateup_weight(0)
+    y = run(lib, xb, wb)
+    rows = sample_rows(T)
+    check(f64(y[rows.tolist()]), xb, wb, rows=rows, label=f"T{T} sampled rows")
+
+
+def test_chunks_equal_whole_prompt_rows(lib):
+    """Eight 2,048-token chunks give the same bits as the rows of the 16,384-token
+    prompt at once (the same k-steps for every element, wherever its row sits)."""
+    torch = lib[2]
+    wb = I.gateup_weight(0)
+    whole = run(lib, I.gateup_tokens(0, 16384), wb)
+    for c in range(8):
+        part = run(lib, I.gateup_tokens(0, 2048, 2048 * c), wb)
+        assert torch.equal(part.view(torch.int16), whole[2048 * c:2048 * (c + 1)].view(torch.int16)), c
+
+
+def test_shapes_and_sizes_are_refused(lib):
+    ppas, step, torch = lib
+    x = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((9, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):                          # odd weight rows
+        ppas.gateup_act(x, w, torch.zeros((4, 4), dtype=torch.bfloat16, device="cuda"))
+    w = torch.zeros((8, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):                          # y must be [T, I]
+        ppas.gateup_act(x, w, torch.zeros((4, 8), dtype=torch.bfloat16, device="cuda"))
+    ppas.gateup_act(x[:0], w, torch.zeros((0, 4), dtype=torch.bfloat16, device="cuda"))   # no tokens
+    x = torch.zeros((4, 96), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((8, 96), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ppas.PPASError) as ex:
+        ppas.gateup_act(x, w, torch.zeros((4, 4), dtype=torch.bfloat16, device="cuda"))
+    assert ex.value.status == ppas.PPAS_EUNSUPPORTED
