@@ -447,9 +447,11 @@ def run_serving_sim_workload(args):
     """The paper's evaluation trace in seconds (Section 4.1, Fig. 2: five 10 s phases,
     steady 0.2 requests/s alternating with a swept burst rate, Poisson arrivals;
     25k-token prompts, 32 outputs) under P-PAS (16,384 / 2,048 by prefill pressure) and
-    fixed 16,384 and 2,048 budgets. Each iteration's duration is measured on the GPU as it
+    fixed budgets of 16,384 and 2,048 tokens and the paper's other static budgets (1k, 4k,
+    8k; --extra-budgets). Each iteration's duration is measured on the GPU as it
     is scheduled: one decoder layer's kernels (QKV projection, rotary embedding + page
-    write, attention, output, gate-up and down projections) times 36 layers
+    write, attention, output, gate-up projection with its gated activation, down
+    projection) times 36 layers
     (layer_cost.DecoderLayerCost). Reports mean and P95 end-to-end latency, TTFT and TPOT
     per rate and rule, and the paper's geometric-mean ratios of P-PAS to each fixed rule."""
     import numpy as np
@@ -461,6 +463,14 @@ def run_serving_sim_workload(args):
     rates = [float(x) for x in args.burst_rates.split(",")]
     seeds = list(range(args.seed, args.seed + args.seeds))
     rules = {"ppas": ("ppas", 16384), "fixed16384": ("fixed", 16384), "fixed2048": ("fixed", 2048)}
+    # the paper's other static budgets (its appendix table: MBT 1k, 4k, 8k)
+    for b in (int(x) for x in args.extra_budgets.split(",") if x):
+        rules[f"fixed{b}"] = ("fixed", b)
+    # P-PAS with other (B_max, B_cap) pairs under the same global budget: the paper's
+    # values define its evaluated configuration, not the policy (Section 3)
+    for pair in (x for x in args.ppas_budgets.split(",") if x):
+        bm, bc = (int(v) for v in pair.split(":"))
+        rules[f"ppas{bm}-{bc}"] = ("ppas", 16384, bm, bc)
     results, parts = {}, {}
     t_start = time.perf_counter()
     from paper_2608_15171_amd.inputs import Seq, StepSpec
@@ -476,8 +486,9 @@ def run_serving_sim_workload(args):
             while time.perf_counter() - t0 < args.warmup_seconds:
                 cost.layer_ms(warm)
             cost.parts_ms = {k: 0.0 for k in cost.parts_ms}
-            for name, (mode, mbt) in rules.items():
-                res = S.simulate(reqs, cost, mode=mode, mbt=mbt)
+            for name, (mode, mbt, *bb) in rules.items():
+                kw = {"b_max": bb[0], "b_cap": bb[1]} if bb else {}
+                res = S.simulate(reqs, cost, mode=mode, mbt=mbt, **kw)
                 per_seed[name].append(S.summarize(res))
                 print(f"serving-sim rate {rate} seed {seed} {name}: {len(res.iterations)} iterations, mean e2e "
                       f"{per_seed[name][-1]['e2e_s']['mean']:.3f} s ({time.perf_counter() - t_start:.0f} s)",
@@ -509,6 +520,14 @@ def run_serving_sim_workload(args):
             "avg_tpot": round(S.geomean_ratio(metric("ppas", "tpot_s", "mean"), metric(base, "tpot_s", "mean")), 4)}
     e16, e2 = metric("fixed16384", "e2e_s", "mean"), metric("fixed2048", "e2e_s", "mean")
     better = ["16k" if a < b else "2k" for a, b in zip(e16, e2)]
+    fixed = sorted((n for n in rules if n.startswith("fixed")), key=lambda n: rules[n][1])
+    best_fixed = [min(fixed, key=lambda n: results[r][n]["e2e_s"]["mean"]) for r in rates]
+    for name in rules:
+        if name.startswith("ppas") and name != "ppas":
+            for base in ("fixed16384", "fixed2048") + tuple(f for f in fixed if f not in ("fixed16384", "fixed2048")):
+                ratios[f"{name}_vs_{base}"] = {
+                    "avg_latency": round(S.geomean_ratio(metric(name, "e2e_s", "mean"), metric(base, "e2e_s", "mean")), 4),
+                    "p95_latency": round(S.geomean_ratio(metric(name, "e2e_s", "p95"), metric(base, "e2e_s", "p95")), 4)}
     ppas_mean = metric("ppas", "e2e_s", "mean")
     rec = {
         "metric": "serving simulation: mean end-to-end request latency under P-PAS (geometric mean over burst rates)",
@@ -519,12 +538,18 @@ def run_serving_sim_workload(args):
                    "burst_rates": rates, "prompt_tokens": 25000, "output_tokens": 32, "layers": 36,
                    "model_shape": "Qwen2.5-3B (hidden 2048, intermediate 11008, 16q/2kv heads, head_dim 128)",
                    "iteration_cost": "one decoder layer measured per iteration x 36: QKV, rope+page write, "
-                                     "attention (+merge), o, gate-up, down; norms, SiLU-mul, residuals, "
-                                     "LM head not included", "seeds": seeds},
+                                     "attention (+merge), o, gate-up with silu(gate)*up in its epilogue, "
+                                     "down; norms, residuals, LM head not included", "seeds": seeds,
+                   "budgets": {n: list(v) for n, v in rules.items()}},
         "results": {str(r): {k: {m: (None if v[m] is None else {s: round(x, 4) for s, x in v[m].items()})
                                  if isinstance(v[m], dict) or v[m] is None else v[m]
                                  for m in v} for k, v in results[r].items()} for r in rates},
         "lower_latency_fixed_rule_per_rate": dict(zip([str(r) for r in rates], better)),
+        "lowest_latency_fixed_budget_per_rate": dict(zip([str(r) for r in rates], best_fixed)),
+        "vs_best_fixed_per_rate": {name: {str(r): round(results[r][name]["e2e_s"]["mean"]
+                                                        / results[r][b]["e2e_s"]["mean"], 4)
+                                          for r, b in zip(rates, best_fixed)}
+                                   for name in rules if name.startswith("ppas")},
         "crossover": better[0] == "16k" and "2k" in better,
         "ratios": ratios,
         "kernel_ms_per_layer_summed": {str(r): parts[r] for r in rates},
@@ -802,6 +827,10 @@ def main():
     ap.add_argument("--burst-rates", default="1,2,3,4,5",
                     help="serving-sim workload: burst-phase arrival rates (requests/s)")
     ap.add_argument("--seeds", type=int, default=3, help="serving-sim workload: traces per rate (seeds 0..n-1)")
+    ap.add_argument("--extra-budgets", default="1024,4096,8192",
+                    help="serving-sim workload: further fixed token budgets beside 2,048 and 16,384")
+    ap.add_argument("--ppas-budgets", default="8192:4096,8192:2048,16384:4096",
+                    help="serving-sim workload: further P-PAS (B_max:B_cap) pairs beside 16384:2048")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the mixed-step attention path has no "

@@ -134,3 +134,20 @@ def test_mbt_crossover_with_a_chunk_efficiency_cost_model():
     assert out[5.0]["2k"] < out[5.0]["16k"]
     for rate in out:
         assert out[rate]["ppas"] <= max(out[rate]["16k"], out[rate]["2k"]) + 1e-9
+
+
+@pytest.mark.parametrize("b_max,b_cap", [(8192, 4096), (16384, 4096), (8192, 2048)])
+def test_other_budget_pairs_bound_every_iteration(b_max, b_cap):
+    """P-PAS with other (B_max, B_cap) pairs under the 16,384-token global budget: no
+    iteration schedules more prefill tokens than B_max, and under pressure (at least
+    N_th prefills and a decode) none more than B_cap; both budgets are used."""
+    reqs = S.bursty_arrivals(2, burst_rate=3.0, prompt_range=(4000, 12000), output_range=(2, 12))
+    res = S.simulate(reqs, cost_model, mode="ppas", mbt=16384, b_max=b_max, b_cap=b_cap)
+    assert set(res.finish) == {r.req_id for r in reqs}
+    for it in res.iterations:
+        assert it.prefill_tokens <= b_max
+        if it.n_prefill >= PT.N_TH and it.n_decode > 0:
+            assert it.budget == b_cap and it.prefill_tokens <= b_cap
+        else:
+            assert it.budget == b_max
+    assert {it.budget for it in res.iterations} == {b_max, b_cap}
