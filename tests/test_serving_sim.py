@@ -141,8 +141,8 @@ def test_other_budget_pairs_bound_every_iteration(b_max, b_cap):
     """P-PAS with other (B_max, B_cap) pairs under the 16,384-token global budget: no
     iteration schedules more prefill tokens than B_max, and under pressure (at least
     N_th prefills and a decode) none more than B_cap; both budgets are used."""
-    reqs = S.bursty_arrivals(2, burst_rate=3.0, prompt_range=(4000, 12000), output_range=(2, 12))
-    res = S.simulate(reqs, cost_model, mode="ppas", mbt=16384, b_max=b_max, b_cap=b_cap)
+    reqs = S.bursty_arrivals(2, burst_rate=20.0, prompt_range=(4000, 12000), output_range=(2, 12))
+    res = S.simulate(reqs, lambda spec: 5 * cost_model(spec), mode="ppas", mbt=16384, b_max=b_max, b_cap=b_cap)
     assert set(res.finish) == {r.req_id for r in reqs}
     for it in res.iterations:
         assert it.prefill_tokens <= b_max
