@@ -154,6 +154,68 @@ def warm_up(step, args):
             return n
 
 
+def attainable_peaks(args):
+    """Ceilings measured on this device, beside the spec peaks: the HBM read rate of a plain
+    streaming read (ppas_stream_read over two 2 GiB buffers in turn, far past the 256 MB
+    Infinity Cache; kernel time from its launch's events) and hipBLASLt's dense bf16 GEMM
+    (torch.matmul, 16384 x 16384 x 16384). Medians of the timed calls after a warm-up of
+    --warmup-seconds each."""
+    import numpy as np
+    import torch
+
+    from paper_2608_15171_amd import ppas
+    from paper_2608_15171_amd.hip_events import HipEvents
+
+    hip = HipEvents()
+    nbytes = 2 << 30
+    bufs = [torch.full((nbytes,), i + 1, dtype=torch.uint8, device="cuda") for i in range(2)]
+    sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+    warm = argparse.Namespace(warmup=-1, warmup_seconds=args.warmup_seconds)
+    warm_up(lambda i: ppas.stream_read(bufs[i % 2], sink), warm)
+    ev = [(hip.create(), hip.create()) for _ in range(20)]
+    for i, (a, b) in enumerate(ev):
+        ppas.stream_read(bufs[i % 2], sink, ppas.events(a, b))
+    torch.cuda.synchronize()
+    read_us = float(np.median([hip.elapsed_ms(a, b) * 1e3 for a, b in ev]))
+    for a, b in ev:
+        hip.destroy(a)
+        hip.destroy(b)
+    del bufs, sink
+    n = 16384
+    g = torch.Generator(device="cuda").manual_seed(0)
+    A = torch.randn((n, n), device="cuda", dtype=torch.bfloat16, generator=g)
+    B = torch.randn((n, n), device="cuda", dtype=torch.bfloat16, generator=g)
+    C = torch.empty((n, n), device="cuda", dtype=torch.bfloat16)
+    warm_up(lambda i: torch.matmul(A, B, out=C), warm)
+    tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+    for a, b in tev:
+        a.record()
+        torch.matmul(A, B, out=C)
+        b.record()
+    torch.cuda.synchronize()
+    gemm_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in tev]))
+    del A, B, C
+    torch.cuda.empty_cache()
+    gbps = nbytes / (read_us * 1e-6) / 1e9
+    tflops = 2.0 * n ** 3 / (gemm_us * 1e-6) / 1e12
+    return {"hbm_read_gbps": round(gbps, 1), "hbm_read_frac_of_spec": round(gbps / PEAK_GBPS, 4),
+            "mfma_gemm_tflops": round(tflops, 1), "mfma_gemm_frac_of_spec": round(tflops / PEAK_TFLOPS, 4),
+            "read": "ppas_stream_read: 2 GiB contiguous, 16-byte nontemporal loads, two buffers in turn; "
+                    f"median of 20 launches, {read_us:.1f} us each",
+            "gemm": f"torch.matmul (hipBLASLt) bf16 {n}x{n}x{n}; median of 10 calls, {gemm_us:.0f} us each"}
+
+
+def with_attainable(rec, att):
+    """Adds the fraction of the measured ceiling of the record's bound to its roofline."""
+    if att is None or "roofline" not in rec:
+        return rec
+    r = rec["roofline"]
+    ceil = att["hbm_read_gbps"] if r["bound"] == "hbm" else att["mfma_gemm_tflops"]
+    r["attainable"] = ceil
+    r["frac_of_attainable"] = round(r["achieved"] / ceil, 4)
+    return rec
+
+
 def parity_summary(out, ref, rows):
     """Max and mean |GPU - oracle| over the oracle's sample rows of the timed step."""
     import numpy as np
@@ -393,6 +455,30 @@ def run_gateup_workload(args, T, act=False):
                      "kernel_us_min": round(min(sum(p) for p in t_whole), 2),
                      "per_launch": {"flop": F, "bytes": B}},
     }
+    if not args.no_attainable:
+        # hipBLASLt on the same projection (the activation, if any, not applied), the same
+        # rotated weight copies and the same warm-up
+        yb = y if not act else torch.empty((Tmax, N), dtype=torch.bfloat16, device="cuda")
+
+        def blas(i):
+            torch.matmul(x, ws[i % copies].t(), out=yb)
+
+        warm_up(blas, args)
+        tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+        for i, (a, b) in enumerate(tev):
+            a.record()
+            blas(i)
+            b.record()
+        torch.cuda.synchronize()
+        blas_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in tev]))
+        del yb
+        rec["hipblaslt_same_shape"] = {
+            "us": round(blas_us, 2), "tflops": round(F / (blas_us * 1e-6) / 1e12, 2),
+            "ours_time_over_hipblaslt": round(us / blas_us, 4),
+            "call": f"torch.matmul(x, w.t()) bf16 [{Tmax}, {H}] x [{H}, {N}]" + (", projection only" if act else "")}
+        att = attainable_peaks(args)
+        rec["attainable"] = att
+        with_attainable(rec, att)
     if T == 0:
         chunks = [(2048 * c, 2048) for c in range(8)]
         warm_up(lambda i: launch(i, chunks[i % 8]), args)
@@ -788,6 +874,7 @@ def measure_step(args, workload: str, with_cpu: bool):
             # attention of the step, dispatch gap included
             "attn_with_merge_us": round(span * 1e3, 2),
             "attn_with_merge_frac": round(step_attn / peak, 4),
+            "attn_kernel_us_median": round(float(np.median(attn_ms)) * 1e3, 2),
             "kv_append_us": round(float(np.mean(app_ms)) * 1e3, 2),
             "tflops_in_kernel": round(F / (k_ms * 1e-3) / 1e12, 2),
             "mfma_frac": round(F / (k_ms * 1e-3) / 1e12 / PEAK_TFLOPS, 4),
@@ -796,6 +883,8 @@ def measure_step(args, workload: str, with_cpu: bool):
             "prefill_tflops_in_kernel": round(M.flops(spec, "prefill") / (k_ms * 1e-3) / 1e12, 2),
             "decode_kv_gbps_in_kernel": round(M.kv_bytes(spec, "decode") / (k_ms * 1e-3) / 1e9, 2),
             "step_roofline_us": round(max(t_flop, t_byte) * 1e6, 2),
+            # max(F / F_peak, B / B_peak) over the kernel's time: the roofline fraction
+            "roofline_frac": round(max(t_flop, t_byte) / (k_ms * 1e-3), 4),
         },
     }
     if with_cpu:
@@ -818,6 +907,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-attainable", action="store_true",
+                    help="skip measuring this device's HBM read and bf16 GEMM ceilings")
     ap.add_argument("--layers", type=int, default=36, help="trace workload: layers")
     ap.add_argument("--trace-mode", choices=["ppas", "fixed"], default="ppas", help="trace workload: budget policy")
     ap.add_argument("--trace-mbt", type=int, default=16384, help="trace workload: global token budget")
@@ -859,6 +950,12 @@ def main():
         sec = measure_step(args, args.secondary, not args.no_cpu_baseline)
         rec["secondary"] = {k: sec[k] for k in ("config", "value", "unit", "ms_per_step", "steps", "warmup",
                                                  "roofline", "breakdown", "cpu_baseline", "parity") if k in sec}
+    if not args.no_attainable:
+        att = attainable_peaks(args)
+        rec["attainable"] = att
+        with_attainable(rec, att)
+        if "secondary" in rec:
+            with_attainable(rec["secondary"], att)
     print(json.dumps(rec), flush=True)
 
 

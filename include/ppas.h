@@ -369,6 +369,21 @@ ppas_status ppas_gateup_act(const void* x, const void* w, void* y, int32_t n_tok
 size_t ppas_gateup_act_workspace_bytes(int32_t n_tokens, int32_t hidden, int32_t n_inter);
 
 /*
+ * A plain streaming read of `bytes` bytes of device memory at `buf`: the
+ * device's attainable HBM read rate, the measured ceiling beside the spec peak
+ * for the memory-bound kernels above (the library's own measurement aid, not a
+ * step of the method). Every 16-byte word is read once with nontemporal loads by
+ * one 256-thread workgroup per compute unit, each wave reading contiguous 8 KB
+ * runs; the XOR of all words, as four uint32 lanes, is XORed into the 16 bytes
+ * of device memory at `sink` (zero it first to receive the XOR itself), so the
+ * reads cannot be elided and the result is checkable. `buf` and `bytes` must be multiples of 16 and `sink`
+ * 4-byte aligned (PPAS_EINVAL otherwise); bytes == 0 is a no-op. Enqueued on
+ * hip_stream without a host sync; the launch records `events` if given.
+ */
+ppas_status ppas_stream_read(const void* buf, size_t bytes, void* sink, const ppas_events* events,
+                             void* hip_stream);
+
+/*
  * For callers that cannot allocate memory: code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc. Computes exactly what
  * ppas_attn_step computes, with the same plan and kernels (bit-identical

@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libppas.so")
 
-SOURCES = ["api.cpp", "plan.cpp", "attn_step.hip", "kv_append.hip", "rope_append.hip", "noalloc.hip", "gateup.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "attn_step.hip", "kv_append.hip", "rope_append.hip", "noalloc.hip", "gateup.hip", "stream_read.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -544,6 +545,26 @@ ppas_status ppas_gateup_act(const void* x, const void* w, void* y, int32_t n_tok
     const int32_t n_out = act_rows(n_inter);
     if (n_out < 0) return PPAS_EINVAL;
     return gateup_call(x, w, y, n_tokens, hidden, n_out, true, workspace, workspace_bytes, events, hip_stream);
+  } catch (...) {
+    return PPAS_EINVAL;
+  }
+}
+
+ppas_status ppas_stream_read(const void* buf, size_t bytes, void* sink, const ppas_events* events,
+                             void* hip_stream) {
+  try {
+    const ppas_status st = check_events(events);
+    if (st != PPAS_OK) return st;
+    if (!buf || !sink || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0 ||
+        reinterpret_cast<uintptr_t>(sink) % 4 != 0)
+      return PPAS_EINVAL;
+    if (bytes == 0) return PPAS_OK;
+    const DeviceInfo dev = current_device();
+    if (!dev.gfx950) return PPAS_EUNSUPPORTED;
+    const hipError_t e = launch_stream_read(buf, bytes, static_cast<uint32_t*>(sink), dev.cus,
+                                            static_cast<hipStream_t>(hip_stream), ev_of(events, 0),
+                                            ev_of(events, 1));
+    return e == hipSuccess ? PPAS_OK : PPAS_EHIP;
   } catch (...) {
     return PPAS_EINVAL;
   }

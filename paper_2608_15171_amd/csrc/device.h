@@ -43,4 +43,9 @@ int64_t gateup_tiles(int32_t T, int32_t N2);
 int gateup_splits(int32_t T, int32_t H, int32_t N2, int cus);
 size_t gateup_workspace_bytes(int32_t T, int32_t N2, int splits);
 
+// XOR of every 16-byte word of buf (bytes a multiple of 16) into sink[0..3],
+// read once by a streaming grid of up to `cus` workgroups.
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int cus, hipStream_t stream,
+                              hipEvent_t ev_start, hipEvent_t ev_stop);
+
 }  // namespace ppas

@@ -99,6 +99,8 @@ _lib.ppas_gateup_act.restype = ctypes.c_int
 _lib.ppas_gateup_act.argtypes = [_vp, _vp, _vp, _i32, _i32, _i32, _vp, _sz, _E, _vp]
 _lib.ppas_gateup_act_workspace_bytes.restype = _sz
 _lib.ppas_gateup_act_workspace_bytes.argtypes = [_i32, _i32, _i32]
+_lib.ppas_stream_read.restype = ctypes.c_int
+_lib.ppas_stream_read.argtypes = [_vp, _sz, _vp, _E, _vp]
 _lib.ppas_plan_items.restype = _i32
 _lib.ppas_plan_items.argtypes = [_P, _vp, _i32, _O, _vp, _i32]
 _lib.ppas_step_plan_create.restype = ctypes.c_int
@@ -309,6 +311,18 @@ def gateup_act(x, w, y, workspace=None, events: Events | None = None, stream=Non
     st = _lib.ppas_gateup_act(_dev(x, "x"), _dev(w, "w"), _dev(y, "y"), T, H, N // 2, _dev(workspace, "workspace"),
                               ws_bytes, None if events is None else ctypes.byref(events), _stream(stream))
     _check(st, "ppas_gateup_act")
+
+
+def stream_read(buf, sink, events: Events | None = None, stream=None) -> None:
+    """A plain streaming read of the whole of `buf` (a contiguous device tensor, a multiple of
+    16 bytes): the XOR of its 16-byte words, as four 32-bit lanes, is XORed into `sink` (a
+    device tensor of 16 bytes). The measured HBM read ceiling of the device."""
+    nbytes = buf.numel() * buf.element_size()
+    if sink.numel() * sink.element_size() != 16:
+        raise ValueError("sink must hold 16 bytes")
+    st = _lib.ppas_stream_read(_dev(buf, "buf"), nbytes, _dev(sink, "sink"),
+                               None if events is None else ctypes.byref(events), _stream(stream))
+    _check(st, "ppas_stream_read")
 
 
 def plan_opts(prefill_split: int = 0, decode_split: int = 0, tile_positions: int = 0, num_cus: int = 0) -> PlanOpts:

@@ -203,6 +203,19 @@ def test_gateup_act_validates_before_any_device_work():
     assert f(1, 1, 1, 4, 64, 4, None, 0, ctypes.byref(half), None) == ppas.PPAS_EINVAL
 
 
+def test_stream_read_validates_before_any_device_work():
+    """Only argument errors and the empty read: each returns before the device is touched."""
+    f = ppas._lib.ppas_stream_read
+    assert f(16, 0, 16, None, None) == ppas.PPAS_OK                  # nothing to read
+    assert f(16, 24, 16, None, None) == ppas.PPAS_EINVAL             # not whole 16-byte words
+    assert f(8, 16, 16, None, None) == ppas.PPAS_EINVAL              # buffer not 16-byte aligned
+    assert f(16, 16, 2, None, None) == ppas.PPAS_EINVAL              # sink not 4-byte aligned
+    assert f(None, 16, 16, None, None) == ppas.PPAS_EINVAL
+    assert f(16, 16, None, None, None) == ppas.PPAS_EINVAL
+    half = ppas.events(start=1)
+    assert f(16, 0, 16, ctypes.byref(half), None) == ppas.PPAS_EINVAL
+
+
 def test_gateup_act_workspace_is_the_projection_s():
     """The activated projection splits like the projection of its 2 n_inter weight rows
     (its partials keep the weight-row layout)."""

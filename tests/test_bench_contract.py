@@ -58,3 +58,12 @@ def test_default_line_is_the_16k_chunk_with_the_pressure_step_beside_it():
     assert sec["config"]["workload"] == "pressure-2x1024+48dec"
     assert sec["roofline"]["bound"] == "hbm" and 0 < sec["roofline"]["frac"] < 1
     assert "merge_kernel_us" in sec["breakdown"] and "attn_with_merge_us" in sec["breakdown"]
+    # the ceilings measured on the same device, and each record's share of its own
+    att = rec["attainable"]
+    assert 2000 < att["hbm_read_gbps"] < 8000 and 300 < att["mfma_gemm_tflops"] < 2500
+    for r, ceil in ((rec, att["mfma_gemm_tflops"]), (sec, att["hbm_read_gbps"])):
+        assert r["roofline"]["attainable"] == ceil
+        assert abs(r["roofline"]["frac_of_attainable"] - r["roofline"]["achieved"] / ceil) < 1e-3
+        b = r["breakdown"]
+        assert b["attn_kernel_us_min"] <= b["attn_kernel_us_median"]
+        assert abs(b["roofline_frac"] - b["step_roofline_us"] / b["attn_kernel_us"]) < 2e-3
