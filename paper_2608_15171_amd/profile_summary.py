@@ -18,6 +18,8 @@ Usage: python -m paper_2608_15171_amd.profile_summary <workload> <dir> <calib_di
        (matrix-core utilisation from one counter pass: profiles/<kernel>.<workload>.mfma.md)
        python -m paper_2608_15171_amd.profile_summary --cache <workload> <dir>
        (L2 hit rate of the gate-up kernel from one counter pass: profiles/gateup_kernel.<workload>.cache.md)
+       python -m paper_2608_15171_amd.profile_summary --read <dir> <calib_dir>
+       (the streaming read that sets the measured HBM ceiling: profiles/stream_read_kernel.read-2GiB.md)
 """
 from __future__ import annotations
 
@@ -269,8 +271,61 @@ def cache_summary(workload: str, d: str, kernel: str = "gateup_kernel", xcds: in
     print(out)
 
 
+def read_summary(d: str, calib: str, workload: str = "mixed512"):
+    """The streaming read that sets the measured HBM ceiling (stream_read_kernel, 2 GiB per
+    launch, run by bench.py after its timed steps): its kernel-trace average and its
+    FETCH_SIZE / WRITE_SIZE per launch, scaled like every traffic figure, which also
+    checks that scaling on a kernel whose bytes are known exactly."""
+    kernel = "stream_read_kernel"
+    stats = list(csv.DictReader(open(os.path.join(d, "trace", "run_kernel_stats.csv"))))
+    bench = json.loads(open(os.path.join(d, "trace_bench.json")).read().strip().splitlines()[-1])
+    row = [r for r in stats if kernel in r["Name"]][0]
+    fetch_kib, nf = counter_per_dispatch(os.path.join(d, "FETCH_SIZE", "run_counter_collection.csv"), kernel, "FETCH_SIZE")
+    write_kib, nw = counter_per_dispatch(os.path.join(d, "WRITE_SIZE", "run_counter_collection.csv"), kernel, "WRITE_SIZE")
+    mib = 1024
+    copy_bytes = mib * 1024 * 1024
+    cf, _ = counter_per_dispatch(os.path.join(calib, "FETCH_SIZE", "run_counter_collection.csv"), "UnaryFunctor", "FETCH_SIZE")
+    cw, _ = counter_per_dispatch(os.path.join(calib, "WRITE_SIZE", "run_counter_collection.csv"), "UnaryFunctor", "WRITE_SIZE")
+    ffac, wfac = copy_bytes / (cf * 1024), copy_bytes / (cw * 1024)
+    nbytes = 2 << 30
+    tr_us = float(row["AverageNs"]) / 1e3
+    att = bench["attainable"]
+    cmd = f"bench.py --workload {workload} --secondary none --no-cpu-baseline"
+    lines = [f"# {kernel} -- the measured HBM read ceiling (2 GiB per launch)", "",
+             "A plain streaming read of a 2 GiB device buffer (ppas_stream_read; each wave reads contiguous 8 KB runs "
+             "with nontemporal 16-byte loads, one 256-thread workgroup per CU) on one MI355X (gfx950), launched by "
+             "bench.py after its timed steps, alternating between two buffers.", "",
+             "## Kernel trace (rocprofv3 --kernel-trace --stats)", "", "Command:", "",
+             f"    cd /tmp && TMPDIR=/tmp rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o run -- "
+             f"python3 <repo>/{cmd}", "",
+             "| kernel | calls | average (us) | min (us) | read rate at the average |", "|---|---|---|---|---|",
+             f"| {kernel} | {row['Calls']} | {tr_us:.2f} | {float(row['MinNs']) / 1e3:.2f} | "
+             f"{nbytes / (tr_us * 1e-6) / 1e12:.2f} TB/s |", "",
+             f"bench.py in the same run, HIP events recorded by the launch: {att['hbm_read_gbps'] / 1e3:.2f} TB/s "
+             f"(median of its 20 timed launches), {100 * att['hbm_read_frac_of_spec']:.1f} % of the 8 TB/s spec peak.",
+             "", "## HBM traffic (rocprofv3 --pmc, one counter per run)", "", "Commands:", ""]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        lines.append(f"    cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- "
+                     f"python3 <repo>/{cmd} --steps 3 --warmup 1")
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        lines.append(f"    cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {c} --output-format csv -d <out> -o run -- "
+                     f"python3 <repo>/paper_2608_15171_amd/calibrate.py --mib {mib}")
+    lines += ["", f"Calibration as for the other kernels: bytes = FETCH_SIZE x 1024 x {ffac:.3f} and WRITE_SIZE x 1024 x "
+                  f"{wfac:.3f} (a plain copy of {mib} MiB).", "", "| per launch | value |", "|---|---|",
+              f"| FETCH_SIZE (KiB, mean of {nf} launches) | {fetch_kib:.0f} |",
+              f"| WRITE_SIZE (KiB, mean of {nw} launches) | {write_kib:.0f} |",
+              f"| bytes read from memory, scaled | {fetch_kib * 1024 * ffac / 1e9:.3f} GB |",
+              f"| bytes the kernel reads | {nbytes / 1e9:.3f} GB |",
+              f"| scaled / known | {fetch_kib * 1024 * ffac / nbytes:.3f} |", ""]
+    out = os.path.join(ROOT, "profiles", f"{kernel}.read-2GiB.md")
+    open(out, "w").write("\n".join(lines))
+    print(out)
+
+
 if __name__ == "__main__":
-    if sys.argv[1] == "--mfma":
+    if sys.argv[1] == "--read":
+        read_summary(*sys.argv[2:4])
+    elif sys.argv[1] == "--mfma":
         mfma_summary(*sys.argv[2:4])
     elif sys.argv[1] == "--stalls":
         stall_summary(*sys.argv[2:4])
