@@ -106,7 +106,7 @@ def main(workload: str, d: str, calib: str, kernel: str = "attn_step_kernel"):
            "write_factor": wfac, "fetch_kib": fetch_kib, "write_kib": write_kib}
     out = os.path.join(ROOT, "profiles", f"{kernel}.{workload}")
     json.dump(rec, open(out + ".traffic.json", "w"), indent=1)
-    cmd = f"bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline"
+    cmd = f"bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --no-attainable"
     lines = [f"# {kernel} -- workload {wl_name} ({workload})", "",
              describe(kernel, workload), "",
              "## Kernel trace (rocprofv3 --kernel-trace --stats)", "", "Command:", "",
@@ -172,7 +172,7 @@ def mfma_summary(workload: str, d: str, kernel: str = "", simds: int = 1024, xcd
     busy = m["SQ_VALU_MFMA_BUSY_CYCLES"] / (simds * cycles)
     mfma_flop = m["SQ_INSTS_MFMA"] * 32768       # the 32x32x16 bf16 and 16x16x32 bf16 MFMAs both do 2*16384 FLOP
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d <out> -o run "
-           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
+           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --no-attainable --steps 3 --warmup-seconds 0.5")
     lines = [f"# {kernel} -- matrix-core utilisation, workload {bench['config']['workload']} ({workload})", "",
              describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
@@ -217,7 +217,7 @@ def stall_summary(workload: str, d: str, kernel: str = "", cus: int = 256, xcds:
     cycles = m["GRBM_GUI_ACTIVE"] / xcds
     wave = m["SQ_WAVE_CYCLES"]
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(STALL_COUNTERS)} --output-format csv -d <out> -o run "
-           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --steps 3 --warmup 2")
+           f"-- python3 <repo>/bench.py --workload {workload}{_sec(kernel)} --no-cpu-baseline --no-attainable --steps 3 --warmup-seconds 0.5")
     share = lambda k: f"{100 * m[k] / wave:.1f} % of wave time"
     lines = [f"# {kernel} -- where the waves spend their time, workload {bench['config']['workload']} ({workload})", "",
              describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
@@ -258,7 +258,7 @@ def cache_summary(workload: str, d: str, kernel: str = "gateup_kernel", xcds: in
     bench = json.loads(open(os.path.join(d, "CACHE_bench.json")).read().strip().splitlines()[-1])
     hit = m["TCC_HIT_sum"] / max(1.0, m["TCC_HIT_sum"] + m["TCC_MISS_sum"])
     cmd = (f"cd /tmp && TMPDIR=/tmp rocprofv3 --pmc {' '.join(CACHE_COUNTERS)} --output-format csv -d <out> -o run "
-           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --steps 3 --warmup 2")
+           f"-- python3 <repo>/bench.py --workload {workload} --no-cpu-baseline --no-attainable --steps 3 --warmup-seconds 0.5")
     lines = [f"# {kernel} -- L2 hit rate, workload {bench['config']['workload']} ({workload})", "",
              describe(kernel, workload), "", "Command (one counter pass):", "", "    " + cmd, "",
              "| quantity | value | how it is read |", "|---|---|---|",
