@@ -272,7 +272,8 @@ def run_trace_workload(args):
         "trace": {"attention_ms_total": round(res["attn_ms_total"], 3),
                   "kv_append_ms_total": round(res["kv_append_ms_total"], 3),
                   "input_gather_ms_total": round(res["gather_ms_total"], 3),
-                  "wall_ms": round(res["wall_ms"], 1), "attn_launches": res["launches"],
+                  "wall_ms": round(res["wall_ms"], 1), "host_enqueue_ms": round(res["host_enqueue_ms"], 1),
+                  "attn_launches": res["launches"],
                   "flop_total": res["flops"], "decode_kv_bytes_total": res["decode_kv_bytes"],
                   "roofline_ms": round(max(res["flops"] / (PEAK_TFLOPS * 1e12),
                                            res["decode_kv_bytes"] / (PEAK_GBPS * 1e9)) * 1e3, 3),

@@ -15,6 +15,7 @@ host for checking. Token content does not affect timing.
 from __future__ import annotations
 
 import math
+import time
 from dataclasses import dataclass
 
 import numpy as np
@@ -89,6 +90,16 @@ def logical_kv_rows(setup: TraceSetup, req_id: int, layer: int, length: int):
     return setup.base_kv[r] + LAYER_SHIFT * layer + np.arange(length)
 
 
+def _upload(x: np.ndarray, device):
+    """Host array -> device tensor without a host wait: the copy starts from a newly
+    allocated pinned tensor, stream-ordered, so the loop can enqueue the next steps
+    while the GPU runs (a copy from pageable memory would wait for the stream)."""
+    import torch
+    pinned = torch.empty(x.shape, dtype=torch.from_numpy(x[:0]).dtype, pin_memory=True)
+    pinned.numpy()[...] = x
+    return pinned.to(device, non_blocking=True)
+
+
 def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress=None):
     """Run every step of the trace in every layer. `check` lists (step index, layer)
     pairs whose outputs are copied back to the host. Returns a dict of timings and
@@ -107,6 +118,10 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     pools = [(torch.zeros((setup.num_pages, H, D // 8, P, 8), dtype=torch.bfloat16, device=device),
               torch.zeros((setup.num_pages, H, D, P), dtype=torch.bfloat16, device=device)) for _ in range(layers)]
     ev = HipEvents()
+    # every launch's timing events, created before the timed loop (creating them inside
+    # it cost the host ~20 us per layer)
+    n_launch = len(setup.steps) * layers
+    ev_pool = [ev.create() for _ in range(4 * n_launch)]
     attn_events, app_events, gather_events = [], [], []
     checks = {}
     want = set(check)
@@ -116,11 +131,12 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
+    h0 = time.perf_counter()
     for si, st in enumerate(setup.steps):
         desc = st.spec.descriptors()
         rows = [setup.req_index[s.req_id] for s in st.spec.seqs]
         bt_host = np.ascontiguousarray(setup.block_table[rows])
-        bt = torch.from_numpy(bt_host).to(device)
+        bt = _upload(bt_host, device)
         plan = ppas.StepPlan(shape, desc, bt_host)
         if ws.numel() < plan.workspace_bytes:
             ws = torch.empty(plan.workspace_bytes, dtype=torch.uint8, device=device)
@@ -129,8 +145,8 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
         iq0, ikv0 = step_rows(setup, st, 0)
         g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         g0.record()
-        iq = (torch.from_numpy(iq0).to(device)[None, :] + shift).reshape(-1)
-        ikv = (torch.from_numpy(ikv0).to(device)[None, :] + shift).reshape(-1)
+        iq = (_upload(iq0, device)[None, :] + shift).reshape(-1)
+        ikv = (_upload(ikv0, device)[None, :] + shift).reshape(-1)
         q_all = torch.index_select(qb, 0, iq).view(layers, T, I.HQ, D)
         k_all = torch.index_select(kb, 0, ikv).view(layers, T, H, D)
         v_all = torch.index_select(vb, 0, ikv).view(layers, T, H, D)
@@ -138,10 +154,10 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
         gather_events.append((g0, g1))
         for layer in range(layers):
             kp, vp = pools[layer]
-            a0, a1 = ev.create(), ev.create()
+            k = 4 * (si * layers + layer)
+            a0, a1, e0, e1 = ev_pool[k:k + 4]
             plan.kv_append(kp, vp, k_all[layer], v_all[layer], bt, ppas.events(a0, a1))
             app_events.append((a0, a1))
-            e0, e1 = ev.create(), ev.create()
             plan.attn_step(out, q_all[layer], kp, vp, bt, ws, ppas.events(e0, e1))
             attn_events.append((e0, e1))
             if (si, layer) in want:
@@ -150,6 +166,7 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
         if progress and si % 100 == 0:
             progress(si, len(setup.steps))
     t1.record()
+    host_ms = (time.perf_counter() - h0) * 1e3
     torch.cuda.synchronize()
     attn_ms = [ev.elapsed_ms(a, b) for a, b in attn_events]
     app_ms = [ev.elapsed_ms(a, b) for a, b in app_events]
@@ -163,7 +180,7 @@ def run(setup: TraceSetup, banks, layers: int, device="cuda", check=(), progress
     step_ms = (np.asarray(attn_ms) + np.asarray(app_ms)).reshape(len(setup.steps), layers).sum(axis=1)
     return {"attn_ms_total": float(np.sum(attn_ms)), "kv_append_ms_total": float(np.sum(app_ms)),
             "gather_ms_total": float(np.sum(gather_ms)), "step_ms": step_ms,
-            "wall_ms": t0.elapsed_time(t1), "launches": len(attn_ms), "flops": flops,
+            "wall_ms": t0.elapsed_time(t1), "host_enqueue_ms": host_ms, "launches": len(attn_ms), "flops": flops,
             "decode_kv_bytes": dec_bytes, "attn_ms_max": float(np.max(attn_ms)), "checks": checks}
 
 
