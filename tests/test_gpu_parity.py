@@ -273,22 +273,6 @@ def test_attention_full_size_sampled(lib, cfg, tile):
     assert np.isfinite(out).all()
 
 
-def tile_rows(spec, g, tile=32):
-    """Every decode row; for each prefill chunk, the first and last row of every
-    32-position tile (the planner's tiles hold 16 or 32 positions, so this also
-    covers every 16-position tile's first or last row) and one seeded row inside
-    each 32-position tile."""
-    rows = []
-    for qs, n, c in spec.descriptors().tolist():
-        if n == 1:
-            rows.append(qs)
-            continue
-        for t0 in range(0, n, tile):
-            t1 = min(n, t0 + tile)
-            rows += [qs + t0, qs + t1 - 1, qs + int(g.integers(t0, t1))]
-    return sorted(set(rows))
-
-
 @pytest.mark.parametrize("cfg", [2, 4])
 def test_attention_full_size_every_row(lib, cfg):
     """Configs 2 and 4 at full size in the planner's default shape: every output row
@@ -299,15 +283,17 @@ def test_attention_full_size_every_row(lib, cfg):
     compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"config{cfg} every row")
 
 
-def test_attention_16k_chunk_every_tile(lib):
+def test_attention_16k_chunk_every_row(lib):
     """Config 3 (one 16,384-token chunk at offset 8,616) in the planner's default
-    shape: the first and last row of every 32-position tile and a seeded row inside
-    each, against the oracle."""
+    shape: every output row against the oracle, in blocks of 2,048 rows (each block
+    within the gates, so the whole step is too)."""
     spec = I.CONFIGS[3](0)
     data, ds = run_step(lib, spec, 0, spare=0)
-    rows = tile_rows(spec, I.rng(0, 81))
-    print(f"config 3: {len(rows)} rows over {spec.n_rows // 32} tiles", flush=True)
-    compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows, label="config3 per tile")
+    out = ds.out_f64()
+    print(f"config 3: every one of {spec.n_rows} rows", flush=True)
+    for r0 in range(0, spec.n_rows, 2048):
+        rows = np.arange(r0, min(spec.n_rows, r0 + 2048))
+        compare(out, oracle_out(data, ds.shape.scale, rows=rows), rows=rows, label=f"config3 rows {r0}..{rows[-1]}")
 
 
 @pytest.mark.parametrize("name", ["mbt2048-tp2shard", "pressure-tp2shard"])
@@ -346,9 +332,9 @@ def test_real_trace_steps_match_oracle(lib):
     """The 64-request P-PAS serving trace itself (prompts of 20k-30k tokens, 16-64
     outputs, bursts of 4, budgets 16,384 / 2,048 by prefill pressure) through one
     layer's persistent pools: every step runs; the step with the most attention work
-    (per-tile rows; two chunks, one after a 16k cached prefix), the largest step
-    capped at 2,048 prefill tokens with decodes running (every row) and the step
-    with the most decode rows (every row) against the oracle."""
+    (two chunks, one after a 16k cached prefix), the largest step capped at 2,048
+    prefill tokens with decodes running and the step with the most decode rows,
+    every row of each against the oracle."""
     from paper_2608_15171_amd import metrics as M
     from paper_2608_15171_amd import trace_run as TR
     setup = TR.make_setup(0, layers=1)
@@ -368,12 +354,14 @@ def test_real_trace_steps_match_oracle(lib):
           f"({steps[dec].decode_rows} decode)", flush=True)
     res = TR.run(setup, banks, 1, check=check)
     scale = 1.0 / math.sqrt(128.0)
-    for i, label, rows in ((big, "most work", tile_rows(steps[big].spec, I.rng(0, 82))),
-                           (cap, "capped step", None), (dec, "most decode rows", None)):
+    for i, label in ((big, "most work"), (cap, "capped step"), (dec, "most decode rows")):
         data = TR.oracle_inputs(setup, banks, i, 0)
         out = res["checks"][(i, 0)].astype(np.float64)
-        compare(out, oracle_out(data, scale, rows=rows), rows=rows,
-                label=f"trace step {i} ({label}, {len(rows) if rows else steps[i].spec.n_rows} rows)")
+        n = steps[i].spec.n_rows
+        for r0 in range(0, n, 2048):
+            rows = np.arange(r0, min(n, r0 + 2048))
+            compare(out, oracle_out(data, scale, rows=rows), rows=rows,
+                    label=f"trace step {i} ({label}, rows {r0}..{rows[-1]} of {n})")
 
 
 # ------------------------------------------------------------------ one prompt, chunked vs single
