@@ -297,14 +297,13 @@ def test_attention_16k_chunk_every_row(lib):
 
 
 @pytest.mark.parametrize("name", ["mbt2048-tp2shard", "pressure-tp2shard"])
-def test_tp2_shard_full_size_sampled(lib, name):
+def test_tp2_shard_full_size_every_row(lib, name):
     """One GPU's half of the MBT=2048 and pressure steps split two ways by KV head
-    (8 query heads, 1 KV head), at full size, on sampled rows."""
+    (8 query heads, 1 KV head), at full size, every row."""
     spec = I.DIAGNOSTICS[name](0)
     print(f"{name}: rows={spec.n_rows} heads={spec.n_q_heads}/{spec.n_kv_heads}", flush=True)
     data, ds = run_step(lib, spec, 0, spare=0)
-    rows = sample_rows(spec, I.rng(0, 78))
-    compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows, label=f"{name} sampled")
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"{name} every row")
 
 
 # ------------------------------------------------------------------ serving trace
@@ -379,57 +378,49 @@ def test_chunked_prompt_matches_oracle(lib, chunk):
     compare(rp.out_f64(), ref, label=f"prompt 1024 / chunk {chunk}")
 
 
-def test_chunk_replay_full_size_sampled(lib):
-    """The 16,384-token prompt as eight 2,048-token chunks and as one chunk: sampled rows
-    (chunk edges included) of both schedules against the oracle."""
+def test_chunk_replay_full_size_every_row(lib):
+    """The 16,384-token prompt as eight 2,048-token chunks and as one chunk: every row
+    of both schedules against the oracle."""
     from paper_2608_15171_amd import chunk_replay as CR
     rp = CR.Replay(16384, seed=0)
-    g = I.rng(0, 78)
-    rows = {0, 1, 2047, 2048, 2049, 4095, 8191, 8192, 14335, 14336, 16383}
-    rows |= set(int(x) for x in g.integers(0, 16384, size=40))
-    rows = sorted(rows)
     q, desc, ks, vs = rp.oracle_inputs()
-    ref = OA.mixed_step_attention(q, desc, ks, vs, rp.shape.scale, 2, rows=rows, with_abs=True)
+    ref = OA.mixed_step_attention(q, desc, ks, vs, rp.shape.scale, 2, with_abs=True)
     for chunk in (2048, 16384):
         print(f"prompt 16384 / chunk {chunk}", flush=True)
         rp.run(chunk)
         out = rp.out_f64()
         assert np.isfinite(out).all()
-        compare(out, ref, rows=rows, label=f"prompt 16384 / chunk {chunk} sampled {len(rows)} rows")
+        compare(out, ref, label=f"prompt 16384 / chunk {chunk} every row")
 
 
 @pytest.mark.parametrize("decode_split", [0, 1 << 20])
-def test_long_contexts_sampled(lib, decode_split):
+def test_long_contexts_every_row(lib, decode_split):
     """Contexts well beyond the workloads' 30k tokens: a 1,024-token chunk after 120,000
     cached tokens and decode rows at 65,536 and 131,071 cached tokens (decode ranges at the
-    8,192-key cap, also when a larger split is asked for); sampled rows against the oracle."""
+    8,192-key cap, also when a larger split is asked for); every row against the oracle."""
     ppas, step, torch = lib
     seqs = [I.Seq(1, 131071, 0), I.Seq(1, 65536, 1), I.Seq(1024, 120000, 2), I.Seq(1, 5, 3)]
     spec = I.StepSpec("long-context", seqs)
     print(f"long contexts, decode split {decode_split}", flush=True)
     data, ds = run_step(lib, spec, 9, splits=(0, decode_split), spare=0)
-    rows = sample_rows(spec, I.rng(9, 77))
-    ref = oracle_out(data, ds.shape.scale, rows=rows)
+    ref = oracle_out(data, ds.shape.scale)
     out = ds.out_f64()
     assert np.isfinite(out).all()
-    compare(out, ref, rows=rows, label=f"long contexts sampled {len(rows)} rows")
+    compare(out, ref, label=f"long contexts, every one of {spec.n_rows} rows")
 
 
 @pytest.mark.parametrize("splits", [(0, 0), (64, 64)])
 def test_many_requests(lib, splits):
     """A thousand requests in one step: 1,000 decode rows at 0-600 cached tokens and 8
     short chunks, so the work list, the merge list and the partial slots are large (with
-    64-key splits, several thousand merged rows). Every decode row and sampled chunk rows
-    against the oracle."""
+    64-key splits, several thousand merged rows). Every row against the oracle."""
     g = I.rng(13, 79)
     seqs = [I.Seq(1, int(g.integers(0, 601)), i) for i in range(1000)]
     seqs += [I.Seq(int(g.integers(2, 100)), int(g.integers(0, 2000)), 1000 + i) for i in range(8)]
     spec = I.StepSpec("many-requests", seqs)
     print(f"many requests: {len(seqs)} requests, {spec.n_rows} rows, splits {splits}", flush=True)
     data, ds = run_step(lib, spec, 13, splits=splits)
-    rows = sample_rows(spec, I.rng(13, 80))
-    compare(ds.out_f64(), oracle_out(data, ds.shape.scale, rows=rows), rows=rows,
-            label=f"many requests, splits {splits}, {len(rows)} rows")
+    compare(ds.out_f64(), oracle_out(data, ds.shape.scale), label=f"many requests, splits {splits}, every row")
 
 
 @pytest.mark.parametrize("case", ["pressure-decode", "long", "tiny"])
