@@ -67,3 +67,29 @@ def test_default_line_is_the_16k_chunk_with_the_pressure_step_beside_it():
         b = r["breakdown"]
         assert b["attn_kernel_us_min"] <= b["attn_kernel_us_median"]
         assert abs(b["roofline_frac"] - b["step_roofline_us"] / b["attn_kernel_us"]) < 2e-3
+
+
+def _bench_module():
+    import importlib.util
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_fraction_of_the_measured_ceiling_follows_the_bound():
+    """Each record's roofline gains its achieved rate over the measured ceiling of its own
+    bound (the GEMM ceiling for MFMA-bound kernels, the streaming read for HBM-bound ones);
+    a ceiling that failed to measure leaves the record as it was."""
+    b = _bench_module()
+    att = {"hbm_read_gbps": 7200.0, "mfma_gemm_tflops": 1350.0}
+    mf = {"roofline": {"bound": "mfma", "achieved": 1147.5}}
+    hb = {"roofline": {"bound": "hbm", "achieved": 4500.0}}
+    b.with_attainable(mf, att)
+    b.with_attainable(hb, att)
+    assert mf["roofline"]["attainable"] == 1350.0 and mf["roofline"]["frac_of_attainable"] == 0.85
+    assert hb["roofline"]["attainable"] == 7200.0 and hb["roofline"]["frac_of_attainable"] == 0.625
+    failed = {"roofline": {"bound": "mfma", "achieved": 1000.0}}
+    b.with_attainable(failed, {"error": "RuntimeError: no library"})
+    assert failed == {"roofline": {"bound": "mfma", "achieved": 1000.0}}
+    assert b.with_attainable({"value": 1}, att) == {"value": 1}
