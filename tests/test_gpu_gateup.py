@@ -63,7 +63,9 @@ def f64(lib, y):
                                    # split reductions: the decoder layer's other projections at decode and
                                    # chunk sizes (down 11008 -> 2048, QKV 2048 -> 2560, output 2048 -> 2048)
                                    (16, 11008, 2048), (3, 11008, 2050), (100, 2048, 2560), (2048, 11008, 2048),
-                                   (600, 2048, 2048)])
+                                   (600, 2048, 2048),
+                                   # just over one round of workgroups' tiles, 64-row tail tiles among them
+                                   (1125, 128, 15300)])
 @pytest.mark.parametrize("split", [True, False])
 def test_ragged_shapes_every_element(lib, T, H, N, split):
     ppas = lib[0]

@@ -66,7 +66,9 @@ def check(g, xb, wb, rows=None, label=""):
 @pytest.mark.parametrize("T,H,NI", [(1, 64, 1), (5, 64, 150), (31, 128, 17), (257, 128, 256), (300, 192, 260),
                                     (256, 256, 128), (513, 2048, 300), (700, 640, 515),
                                     # split reductions: decode-sized and small-chunk calls
-                                    (16, 2048, 11008), (3, 2048, 1025), (100, 2048, 1280), (2048, 2048, 1024)])
+                                    (16, 2048, 11008), (3, 2048, 1025), (100, 2048, 1280), (2048, 2048, 1024),
+                                    # just over one round of workgroups' tiles, tail tiles among them
+                                    (1125, 128, 7650)])
 @pytest.mark.parametrize("split", [True, False])
 def test_ragged_shapes_every_element(lib, T, H, NI, split):
     ppas = lib[0]
